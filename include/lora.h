@@ -1,0 +1,180 @@
+/*
+ * lora.h - C ABI of the batched, heterogeneous-rank LoRA delta on MI355X (gfx950).
+ *
+ * What is computed.  The paper's Eq. 1 (Section 2.1, "LLM adaption") adapts a
+ * weight W in R^{H1 x H2} by A in R^{H1 x r} and B in R^{r x H2}:
+ * y' = xW + xAB, row vectors.  Section 2.2 keeps one base model and computes
+ * xAB on the fly per request, adding it to the shared xW; Sections 2.3 (C2)
+ * and 4.1 batch many requests of different adapters and ranks into one step,
+ * each token gathering its own adapter.  This library computes, in place,
+ *
+ *     y[t, :] <- round( y[t, :] + s_g * (x[t, :] . A_g) . B_g )
+ *
+ * for every row t of a segment whose adapter is g >= 0, where y = xW is the
+ * caller's base output, s_g a per-adapter float scale (1.0 recovers Eq. 1)
+ * and "round" one round-to-nearest-even of the float32 sum to the storage
+ * dtype.  The rank-r intermediate x.A_g is kept in float32.  Rows of
+ * segments with adapter -1 are never read from x nor written in y.
+ *
+ * A step is described by segments: a decode token is a segment of length 1,
+ * a prompt is one segment of its length (continuous batching, Section 2.2).
+ *
+ * Layout (paper's row-vector convention, Section 2.1):
+ *   x  [n_rows, h_in]  row-major, leading dimension ldx (elements)
+ *   y  [n_rows, h_out] row-major, leading dimension ldy (elements)
+ *   A_g [h_in, r_g]    row-major (dense, leading dimension r_g)
+ *   B_g [r_g, h_out]   row-major (dense, leading dimension h_out)
+ *   v  [n_rows, ldv]   float32, v[t, 0:r_g] = x[t].A_g (shrink result)
+ * 16-bit elements are IEEE binary16 (LORA_F16) or bfloat16 (LORA_BF16).
+ *
+ * Requirements, all checked on the host before anything is enqueued; a
+ * violation returns a negative code, sets lora_last_error() and enqueues
+ * nothing:
+ *   - h_in, h_out, ldx, ldy: positive multiples of 8 (16-byte rows);
+ *     ldx >= h_in, ldy >= h_out; ldv a multiple of 4 with ldv >= the largest
+ *     rank used in the batch;
+ *   - x, y, v, every A_g and B_g: 16-byte aligned device pointers;
+ *   - ranks in [1, 256]; adapter indices in [-1, n_adapters);
+ *   - seg_offset[0] = 0, nondecreasing, seg_offset[n_segments] = n_rows;
+ *   - x and y do not overlap.
+ *
+ * Asynchrony.  Every compute call is enqueued on the caller's HIP stream
+ * (a hipStream_t passed as void*, NULL = the null stream) and returns
+ * without waiting for the GPU.  No call except lora_register_adapters,
+ * lora_plan_create and the destroy/release calls allocates device memory.
+ * Calls are deterministic: the same inputs give the same bits.
+ *
+ * Thread safety.  Distinct tables and plans may be used from any threads.
+ * Calls sharing one workspace or one plan must be ordered (one stream).
+ */
+#ifndef LORA_H
+#define LORA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LORA_ABI_VERSION 1
+
+typedef enum { LORA_F16 = 0, LORA_BF16 = 1 } lora_dtype_t;
+
+enum {
+    LORA_OK = 0,
+    LORA_E_ARG = -1,        /* null pointer, negative count, bad dtype/device   */
+    LORA_E_SHAPE = -2,      /* h / ld not a multiple of 8, ld too small, segments malformed */
+    LORA_E_RANK = -3,       /* rank outside [1, 256]                             */
+    LORA_E_INDEX = -4,      /* adapter index outside [-1, n_adapters)            */
+    LORA_E_ALIGN = -5,      /* pointer not 16-byte aligned                       */
+    LORA_E_NOMEM = -6,      /* host or device allocation failed                  */
+    LORA_E_HIP = -7,        /* a HIP runtime call or kernel launch failed        */
+    LORA_E_WORKSPACE = -8,  /* workspace smaller than lora_workspace_bytes()     */
+    LORA_E_OVERLAP = -9     /* x and y overlap                                   */
+};
+
+/* A step's batch, in HOST memory; read during the call only. */
+typedef struct {
+    int32_t n_rows;             /* rows of x and y in this step                     */
+    int32_t n_segments;
+    const int32_t* seg_offset;  /* [n_segments + 1]                                 */
+    const int32_t* seg_adapter; /* [n_segments], -1 = no adapter for that segment   */
+} lora_batch_t;
+
+typedef struct lora_table_s* lora_table_t; /* adapters of one projection, library-owned */
+typedef struct lora_plan_s* lora_plan_t;   /* a batch planned against a table, library-owned */
+
+/*
+ * Register the adapters of one projection h_in -> h_out (the registry of
+ * adapter ranks and weights of Section 4, kept resident on the device).
+ * A_ptrs[i] / B_ptrs[i] are DEVICE pointers owned by the caller that must stay
+ * valid until lora_release_adapters; ranks[i] in [1,256]; scales[i] is s_i.
+ * The library copies the pointer / rank / scale table into device memory it
+ * owns on `device` (synchronously on `stream`; the host arrays may be freed on
+ * return).  All adapters of one table share dtype, h_in and h_out.
+ * On success *out is a new table; on failure *out is left NULL.
+ */
+int lora_register_adapters(lora_table_t* out, int device, int h_in, int h_out, int dtype,
+                           int n_adapters, const void* const* A_ptrs, const void* const* B_ptrs,
+                           const int32_t* ranks, const float* scales, void* stream);
+
+/* Free the table's device copy. The caller's A/B memory is not touched.
+ * The caller must make sure no enqueued call still uses the table. */
+int lora_release_adapters(lora_table_t t);
+
+/* Bytes of device workspace that lora_shrink / lora_expand / lora_apply_fused
+ * need for this batch (plan, float32 intermediate, split-K partials). */
+int lora_workspace_bytes(lora_table_t t, const lora_batch_t* b, size_t* bytes);
+
+/*
+ * Shrink half of xAB (the gathered x.A_g of Section 4.1's batched operator):
+ * v[t, 0:r_g] = x[t, :] . A_g in float32 for every row with adapter g >= 0.
+ * Rows without an adapter and columns j >= r_g of v are not written.
+ * ws: device workspace of ws_bytes >= lora_workspace_bytes(t, b), any
+ * contents; it is overwritten.
+ */
+int lora_shrink(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, float* v,
+                int64_t ldv, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Expand half and the add into the base output (Eq. 1's xW + xAB):
+ * y[t, :] <- round(y[t, :] + s_g * v[t, 0:r_g] . B_g) for every row with
+ * adapter g >= 0, in place.  v is float32 [n_rows, ldv] on the device.
+ */
+int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t ldv, void* y,
+                int64_t ldy, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The whole delta in one call: y[t,:] <- round(y[t,:] + s_g (x[t,:].A_g).B_g).
+ * The float32 intermediate lives only in ws.  Uploads the plan of this batch
+ * into ws, then runs the kernels; no host synchronisation.
+ */
+int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,
+                     int64_t ldy, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Plan a batch once and apply it many times (the same step's batch applies to
+ * every adapted projection of every layer).  lora_plan_create validates the
+ * batch, builds the rank-bucketed work list on the host and uploads it, with
+ * its own workspace, to device memory owned by the plan (allocates; not for
+ * the hot loop).  lora_plan_apply is lora_apply_fused without the upload: it
+ * enqueues kernels only.  Calls on one plan must be ordered (one stream).
+ */
+int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream);
+int lora_plan_apply(lora_plan_t p, const void* x, int64_t ldx, void* y, int64_t ldy, void* stream);
+int lora_plan_destroy(lora_plan_t p);
+
+/*
+ * The two halves of lora_plan_apply as separate launches (one kernel each),
+ * for callers that schedule them apart or time them one by one:
+ * lora_plan_shrink writes the float32 intermediate x.A_g into the plan's own
+ * workspace; lora_plan_expand adds s_g * v.B_g into y from that workspace.
+ * lora_plan_expand must follow a lora_plan_shrink of the same plan in stream
+ * order; the pair computes exactly what lora_plan_apply computes.
+ */
+int lora_plan_shrink(lora_plan_t p, const void* x, int64_t ldx, void* stream);
+int lora_plan_expand(lora_plan_t p, void* y, int64_t ldy, void* stream);
+
+/*
+ * The integer part of the plan, on the host only (no GPU needed): rows that
+ * carry an adapter, grouped by adapter (Sections 2.3 C2 / 4.1 gather).  Groups
+ * are ordered by the first row that uses the adapter; rows ascend within a
+ * group; adapter -1 rows are dropped.  perm: [n_rows] capacity,
+ * group_off: [n_rows + 1], group_adapter: [n_rows]; *n_groups receives G
+ * and perm[0 .. group_off[G]) is filled.
+ */
+int lora_group_rows(const lora_batch_t* b, int32_t n_adapters, int32_t* perm, int32_t* group_off,
+                    int32_t* group_adapter, int32_t* n_groups);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* lora_last_error(void);
+
+/* LORA_ABI_VERSION of the built library. */
+int lora_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LORA_H */

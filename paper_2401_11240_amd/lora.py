@@ -1,0 +1,222 @@
+"""Thin Python binding of liblora.so (the C ABI in include/lora.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+library.  Device buffers are passed as integer addresses or as objects with a
+``data_ptr()`` method (torch tensors); streams as integer ``hipStream_t``
+handles or objects with a ``cuda_stream`` attribute.  Failures raise
+``LoraError`` carrying the library's code and message.  There is no fallback:
+if the library is not built, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+from . import build as _build
+
+LORA_F16 = 0
+LORA_BF16 = 1
+
+LORA_OK = 0
+LORA_E_ARG = -1
+LORA_E_SHAPE = -2
+LORA_E_RANK = -3
+LORA_E_INDEX = -4
+LORA_E_ALIGN = -5
+LORA_E_NOMEM = -6
+LORA_E_HIP = -7
+LORA_E_WORKSPACE = -8
+LORA_E_OVERLAP = -9
+
+# Every function the header declares (checked by the tests).
+EXPORTS = (
+    "lora_register_adapters", "lora_release_adapters", "lora_workspace_bytes", "lora_shrink",
+    "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
+    "lora_plan_shrink", "lora_plan_expand", "lora_group_rows", "lora_last_error",
+    "lora_abi_version",
+)
+
+
+class LoraError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"liblora error {code}: {message}")
+        self.code = code
+        self.message = message
+
+
+class _Batch(C.Structure):
+    _fields_ = [
+        ("n_rows", C.c_int32),
+        ("n_segments", C.c_int32),
+        ("seg_offset", C.POINTER(C.c_int32)),
+        ("seg_adapter", C.POINTER(C.c_int32)),
+    ]
+
+
+class Batch:
+    """A step's batch: segments (offset, adapter); keeps its arrays alive."""
+
+    def __init__(self, seg_offset, seg_adapter, n_rows: Optional[int] = None):
+        self.seg_offset = np.ascontiguousarray(seg_offset, dtype=np.int32)
+        self.seg_adapter = np.ascontiguousarray(seg_adapter, dtype=np.int32)
+        if self.seg_offset.size == 0:
+            self.seg_offset = np.zeros(1, dtype=np.int32)
+        self.n_rows = int(self.seg_offset[-1]) if n_rows is None else int(n_rows)
+        self._c = _Batch(self.n_rows, int(self.seg_adapter.shape[0]),
+                         self.seg_offset.ctypes.data_as(C.POINTER(C.c_int32)),
+                         self.seg_adapter.ctypes.data_as(C.POINTER(C.c_int32)))
+
+    @property
+    def c(self):
+        return C.byref(self._c)
+
+
+_lib = None
+
+
+def load():
+    """Load the in-tree liblora.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = _build.lib_path()
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run __graft_entry__.build() first")
+    lib = C.CDLL(path)
+    vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    i32p = C.POINTER(C.c_int32)
+    f32p = C.POINTER(C.c_float)
+    sig = {
+        "lora_register_adapters": [C.POINTER(vp), C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                   C.POINTER(vp), C.POINTER(vp), i32p, f32p, vp],
+        "lora_release_adapters": [vp],
+        "lora_workspace_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
+        "lora_shrink": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
+        "lora_expand": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
+        "lora_apply_fused": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
+        "lora_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
+        "lora_plan_apply": [vp, vp, i64, vp, i64, vp],
+        "lora_plan_destroy": [vp],
+        "lora_plan_shrink": [vp, vp, i64, vp],
+        "lora_plan_expand": [vp, vp, i64, vp],
+        "lora_group_rows": [C.POINTER(_Batch), i32, i32p, i32p, i32p, i32p],
+        "lora_last_error": [],
+        "lora_abi_version": [],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    lib.lora_last_error.restype = C.c_char_p
+    _lib = lib
+    return lib
+
+
+def _addr(p) -> int:
+    if p is None:
+        return 0
+    if hasattr(p, "data_ptr"):
+        return int(p.data_ptr())
+    return int(p)
+
+
+def _stream(s) -> int:
+    if s is None:
+        return 0
+    if hasattr(s, "cuda_stream"):
+        return int(s.cuda_stream)
+    return int(s)
+
+
+def _check(rc: int):
+    if rc != LORA_OK:
+        raise LoraError(rc, lora_last_error())
+
+
+def lora_last_error() -> str:
+    return load().lora_last_error().decode()
+
+
+def lora_abi_version() -> int:
+    return int(load().lora_abi_version())
+
+
+def lora_register_adapters(device: int, h_in: int, h_out: int, dtype: int, A_ptrs: Sequence,
+                           B_ptrs: Sequence, ranks: Sequence[int], scales: Sequence[float],
+                           stream=None) -> int:
+    n = len(ranks)
+    A = (C.c_void_p * max(1, n))(*[_addr(p) for p in A_ptrs])
+    B = (C.c_void_p * max(1, n))(*[_addr(p) for p in B_ptrs])
+    r = np.ascontiguousarray(ranks, dtype=np.int32)
+    s = np.ascontiguousarray(scales, dtype=np.float32)
+    out = C.c_void_p()
+    _check(load().lora_register_adapters(C.byref(out), device, h_in, h_out, dtype, n, A, B,
+                                         r.ctypes.data_as(C.POINTER(C.c_int32)),
+                                         s.ctypes.data_as(C.POINTER(C.c_float)), _stream(stream)))
+    return out.value
+
+
+def lora_release_adapters(table: int) -> None:
+    _check(load().lora_release_adapters(table))
+
+
+def lora_workspace_bytes(table: int, batch: Batch) -> int:
+    out = C.c_size_t()
+    _check(load().lora_workspace_bytes(table, batch.c, C.byref(out)))
+    return int(out.value)
+
+
+def lora_shrink(table: int, batch: Batch, x, ldx: int, v, ldv: int, ws, ws_bytes: int,
+                stream=None) -> None:
+    _check(load().lora_shrink(table, batch.c, _addr(x), ldx, _addr(v), ldv, _addr(ws), ws_bytes,
+                              _stream(stream)))
+
+
+def lora_expand(table: int, batch: Batch, v, ldv: int, y, ldy: int, ws, ws_bytes: int,
+                stream=None) -> None:
+    _check(load().lora_expand(table, batch.c, _addr(v), ldv, _addr(y), ldy, _addr(ws), ws_bytes,
+                              _stream(stream)))
+
+
+def lora_apply_fused(table: int, batch: Batch, x, ldx: int, y, ldy: int, ws, ws_bytes: int,
+                     stream=None) -> None:
+    _check(load().lora_apply_fused(table, batch.c, _addr(x), ldx, _addr(y), ldy, _addr(ws),
+                                   ws_bytes, _stream(stream)))
+
+
+def lora_plan_create(table: int, batch: Batch, stream=None) -> int:
+    out = C.c_void_p()
+    _check(load().lora_plan_create(C.byref(out), table, batch.c, _stream(stream)))
+    return out.value
+
+
+def lora_plan_apply(plan: int, x, ldx: int, y, ldy: int, stream=None) -> None:
+    _check(load().lora_plan_apply(plan, _addr(x), ldx, _addr(y), ldy, _stream(stream)))
+
+
+def lora_plan_shrink(plan: int, x, ldx: int, stream=None) -> None:
+    _check(load().lora_plan_shrink(plan, _addr(x), ldx, _stream(stream)))
+
+
+def lora_plan_expand(plan: int, y, ldy: int, stream=None) -> None:
+    _check(load().lora_plan_expand(plan, _addr(y), ldy, _stream(stream)))
+
+
+def lora_plan_destroy(plan: int) -> None:
+    _check(load().lora_plan_destroy(plan))
+
+
+def lora_group_rows(batch: Batch, n_adapters: int):
+    """(perm, group_off, group_adapter) of the library's host-side grouping."""
+    T = max(1, batch.n_rows)
+    perm = np.zeros(T, dtype=np.int32)
+    goff = np.zeros(T + 1, dtype=np.int32)
+    gad = np.zeros(T, dtype=np.int32)
+    G = C.c_int32()
+    p = lambda a: a.ctypes.data_as(C.POINTER(C.c_int32))
+    _check(load().lora_group_rows(batch.c, n_adapters, p(perm), p(goff), p(gad), C.byref(G)))
+    g = int(G.value)
+    return perm[:int(goff[g])].copy(), goff[:g + 1].copy(), gad[:g].copy()

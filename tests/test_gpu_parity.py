@@ -1,0 +1,369 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Small cases compare every output; the five named Llama-shaped workloads run
+at full size in the same launch configuration the benchmark times and are
+checked on sampled rows (the oracle computes rows one by one) plus
+properties that hold at any size.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2401_11240_amd import workloads as W
+
+from parity import compare, compare_v
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():   # collected on CPU-only hosts, never run there
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2401_11240_amd import device as D  # noqa: E402
+from paper_2401_11240_amd import lora as L  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def stream():
+    return torch.cuda.current_stream(DEV)
+
+
+def workspace(table, batch):
+    n = L.lora_workspace_bytes(table, batch)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=DEV), n
+
+
+def run_fused(dw, name):
+    p = dw.projection(name)
+    x = dw.xs[p.x]
+    y = p.y.clone()
+    ws, n = workspace(p.table, dw.batch)
+    L.lora_apply_fused(p.table, dw.batch, x, x.shape[1], y, y.shape[1], ws, n, stream())
+    torch.cuda.synchronize()
+    return D.from_device_bits(y)
+
+
+def oracle_full(w, name):
+    p = w.projection(name)
+    return oracle.lora_apply(w.seg_offset, w.seg_adapter, w.xs[p.x], p.A, p.B, w.ranks, w.scales,
+                             p.y, w.dtype)
+
+
+def int_bits(rng, shape, lo, hi, dtype):
+    return W.to_bits(rng.integers(lo, hi, shape).astype(np.float32), dtype)
+
+
+def make_selector(seed, dtype, h_in, h_out, ranks, seg_lens, seg_adapter):
+    """Selector adapters with integer x and y: every product and sum is exact,
+    so the HIP result must equal the oracle bit for bit."""
+    rng = np.random.default_rng(seed)
+    T = int(np.sum(seg_lens))
+    A, B = [], []
+    for r in ranks:
+        c = int(rng.integers(0, h_in - r + 1))
+        e = int(rng.integers(0, h_out - r + 1))
+        a = np.zeros((h_in, r), np.float32)
+        b = np.zeros((r, h_out), np.float32)
+        a[c + np.arange(r), np.arange(r)] = 1.0
+        b[np.arange(r), e + np.arange(r)] = 1.0
+        A.append(W.to_bits(a, dtype))
+        B.append(W.to_bits(b, dtype))
+    so = np.concatenate([[0], np.cumsum(seg_lens)]).astype(np.int32)
+    w = W.Workload(name=f"selector{seed}", dtype=dtype, n_rows=T, seg_offset=so,
+                   seg_adapter=np.asarray(seg_adapter, np.int32),
+                   ranks=np.asarray(ranks, np.int32),
+                   scales=np.array([2.0 ** int(rng.integers(-2, 3)) for _ in ranks], np.float32),
+                   xs={"x": int_bits(rng, (T, h_in), -8, 9, dtype)},
+                   projections=[W.Projection("p", h_in, h_out, "x", A, B,
+                                             int_bits(rng, (T, h_out), -64, 65, dtype))])
+    return w
+
+
+# ---------------------------------------------------------------------------
+# exact cases
+# ---------------------------------------------------------------------------
+
+def test_hand_worked_example_exact():
+    import json
+    with open(os.path.join(os.path.dirname(__file__), "golden", "tiny_delta.json")) as f:
+        g = json.load(f)
+    # h=2 is below the 16-byte row granule: embed the example in h=8 with zeros.
+    dt = W.F16
+    T = len(g["x"])
+    x = np.zeros((T, 8), np.float32)
+    x[:, :2] = g["x"]
+    y = np.zeros((T, 8), np.float32)
+    y[:, :2] = g["y"]
+    A = []
+    B = []
+    for a, b in zip(g["A"], g["B"]):
+        a = np.asarray(a, np.float32)
+        b = np.asarray(b, np.float32)
+        aa = np.zeros((8, a.shape[1]), np.float32)
+        aa[:2] = a
+        bb = np.zeros((b.shape[0], 8), np.float32)
+        bb[:, :2] = b
+        A.append(W.to_bits(aa, dt))
+        B.append(W.to_bits(bb, dt))
+    w = W.Workload("golden", dt, T, np.asarray(g["seg_offset"], np.int32),
+                   np.asarray(g["seg_adapter"], np.int32), np.asarray(g["ranks"], np.int32),
+                   np.asarray(g["scales"], np.float32), {"x": W.to_bits(x, dt)},
+                   [W.Projection("p", 8, 8, "x", A, B, W.to_bits(y, dt))])
+    dw = D.upload(w, DEV)
+    out = run_fused(dw, "p")
+    dw.release()
+    got = W.bits_to_f32(out, dt)[:, :2]
+    assert got.tolist() == g["out_expected"]
+    assert np.all(W.bits_to_f32(out, dt)[:, 2:] == 0)
+
+
+SELECTOR_CASES = [
+    # (dtype, h_in, h_out, ranks, seg_lens, seg_adapter)
+    (W.F16, 4096, 4096, [8, 8, 8, 8], [1] * 8, [0, 1, 2, 3, 0, 1, 2, 3]),
+    (W.BF16, 4104, 1032, [8, 16, 32, 64, 128, 256], [1, 3, 1, 40, 1, 2, 5, 1],
+     [0, 1, -1, 2, 3, 4, 5, 1]),
+    (W.F16, 520, 2056, [3, 24, 1, 200, 255], [2, 1, 7, 1, 9], [0, 1, 2, 3, 4]),
+    (W.BF16, 8192, 8200, [64, 16], [300, 1, 1, 77], [0, 1, -1, 0]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SELECTOR_CASES)))
+def test_selector_adapters_bit_exact(case):
+    dtype, h_in, h_out, ranks, lens, sa = SELECTOR_CASES[case]
+    say(f"selector case {case}: h_in={h_in} h_out={h_out} ranks={ranks}")
+    w = make_selector(500 + case, dtype, h_in, h_out, ranks, lens, sa)
+    dw = D.upload(w, DEV)
+    got = run_fused(dw, "p")
+    ref = oracle.round_bits(oracle_full(w, "p"), dtype)
+    assert np.array_equal(got, ref)
+    # the shrink alone: v[t, j] = x[t, c_g + j] exactly
+    p = dw.projection("p")
+    r_max = max(ranks)
+    ldv = (r_max + 3) // 4 * 4
+    v = torch.full((w.n_rows, ldv), float("nan"), dtype=torch.float32, device=DEV)
+    ws, n = workspace(p.table, dw.batch)
+    x = dw.xs["x"]
+    L.lora_shrink(p.table, dw.batch, x, x.shape[1], v, ldv, ws, n, stream())
+    torch.cuda.synchronize()
+    vg = v.cpu().numpy()
+    vr = oracle.lora_shrink(w.seg_offset, w.seg_adapter, w.xs["x"], w.projections[0].A, w.ranks,
+                            dtype, ldv=ldv)
+    ra = w.row_adapter()
+    for t in range(w.n_rows):
+        g = ra[t]
+        if g < 0:
+            assert np.all(np.isnan(vg[t]))
+        else:
+            assert np.array_equal(vg[t, :ranks[g]], vr[t, :ranks[g]].astype(np.float32))
+            assert np.all(np.isnan(vg[t, ranks[g]:]))
+    dw.release()
+
+
+# ---------------------------------------------------------------------------
+# random inputs, several tiles and ragged tails
+# ---------------------------------------------------------------------------
+
+RANDOM_CASES = [
+    # seed, dtype, h_in, h_out, n_adapters, rank_set, seg_lens, adapter law
+    (1, W.F16, 4096, 4096, 6, [8, 16, 32, 64], [1] * 24, "zipf"),
+    (2, W.BF16, 1032, 2056, 5, [8, 16, 32, 64, 128, 256], [1, 1, 1, 70, 1, 9, 1, 130, 1], "uniform"),
+    (3, W.F16, 776, 520, 4, [3, 40, 96, 1], [1, 5, 1, 2, 1, 33], "uniform"),
+    (4, W.BF16, 5120, 13824, 8, [8, 16, 32, 64], [1] * 20, "zipf"),
+    (5, W.BF16, 13824, 5120, 8, [8, 16, 32, 64], [1] * 20, "zipf"),
+]
+
+
+def random_workload(case):
+    seed, dtype, h_in, h_out, n_ad, rank_set, lens, law = case
+    rng = np.random.default_rng(seed)
+    if law == "zipf":
+        sa = rng.choice(n_ad, size=len(lens), p=W.zipf_probs(n_ad)).astype(np.int32)
+    else:
+        sa = rng.integers(-1, n_ad, size=len(lens)).astype(np.int32)
+    return W.small_random(seed, dtype=dtype, h_in=h_in, h_out=h_out, n_adapters=n_ad,
+                          rank_set=rank_set, seg_lens=lens, seg_adapter=sa)
+
+
+@pytest.mark.parametrize("case", range(len(RANDOM_CASES)))
+def test_random_parity_fused_shrink_expand(case):
+    c = RANDOM_CASES[case]
+    say(f"random case {case}: {c[:6]}")
+    w = random_workload(c)
+    dw = D.upload(w, DEV)
+    p = dw.projection("proj")
+    got = run_fused(dw, "proj")
+    ref = oracle_full(w, "proj")
+    st = compare(got, ref, w.dtype, f"random case {case}")
+    say("  fused", st)
+    # rows without an adapter are bit-identical to the input
+    none = w.row_adapter() < 0
+    assert np.array_equal(got[none], w.projections[0].y[none])
+
+    # shrink alone vs the oracle's shrink
+    ldv = (int(w.ranks.max()) + 3) // 4 * 4
+    v = torch.zeros((w.n_rows, ldv), dtype=torch.float32, device=DEV)
+    ws, n = workspace(p.table, dw.batch)
+    x = dw.xs["x"]
+    L.lora_shrink(p.table, dw.batch, x, x.shape[1], v, ldv, ws, n, stream())
+    torch.cuda.synchronize()
+    vg = v.cpu().numpy()
+    vr = np.nan_to_num(oracle.lora_shrink(w.seg_offset, w.seg_adapter, w.xs["x"],
+                                          w.projections[0].A, w.ranks, w.dtype, ldv=ldv))
+    mask = np.zeros_like(vr, dtype=bool)
+    ra = w.row_adapter()
+    for t in range(w.n_rows):
+        if ra[t] >= 0:
+            mask[t, :w.ranks[ra[t]]] = True
+    compare_v(np.where(mask, vg, 0.0), np.where(mask, vr, 0.0), f"shrink case {case}")
+
+    # expand alone from a float32 v drawn by the generator's RNG
+    rng = np.random.default_rng(900 + case)
+    v_in = rng.standard_normal((w.n_rows, ldv)).astype(np.float32)
+    y = p.y.clone()
+    vt = torch.from_numpy(v_in).to(DEV)
+    L.lora_expand(p.table, dw.batch, vt, ldv, y, y.shape[1], ws, n, stream())
+    torch.cuda.synchronize()
+    ref_e = oracle.lora_expand(w.seg_offset, w.seg_adapter, v_in, w.projections[0].B, w.ranks,
+                               w.scales, w.projections[0].y, w.dtype)
+    compare(D.from_device_bits(y), ref_e, w.dtype, f"expand case {case}")
+
+    # fused == shrink then expand through the boundary, bit for bit
+    y2 = p.y.clone()
+    L.lora_expand(p.table, dw.batch, v, ldv, y2, y2.shape[1], ws, n, stream())
+    torch.cuda.synchronize()
+    assert np.array_equal(D.from_device_bits(y2), got)
+    dw.release()
+
+
+def test_plan_reuse_and_determinism():
+    w = random_workload(RANDOM_CASES[1])
+    dw = D.upload(w, DEV)
+    p = dw.projection("proj")
+    x = dw.xs["x"]
+    ref = run_fused(dw, "proj")
+    again = run_fused(dw, "proj")
+    assert np.array_equal(ref, again)
+    plan = L.lora_plan_create(p.table, dw.batch, stream())
+    try:
+        for rep in range(3):   # the split-K counters must re-arm between launches
+            y = p.y.clone()
+            L.lora_plan_apply(plan, x, x.shape[1], y, y.shape[1], stream())
+            torch.cuda.synchronize()
+            assert np.array_equal(D.from_device_bits(y), ref), rep
+    finally:
+        L.lora_plan_destroy(plan)
+    dw.release()
+
+
+def test_permutation_invariance_bit_exact():
+    w = random_workload(RANDOM_CASES[0])
+    dw = D.upload(w, DEV)
+    got = run_fused(dw, "proj")
+    dw.release()
+    perm = np.random.default_rng(3).permutation(w.n_rows)
+    w2 = W.Workload(w.name, w.dtype, w.n_rows, w.seg_offset, w.seg_adapter[perm], w.ranks,
+                    w.scales, {"x": w.xs["x"][perm]},
+                    [W.Projection("proj", 4096, 4096, "x", w.projections[0].A,
+                                  w.projections[0].B, w.projections[0].y[perm])])
+    dw2 = D.upload(w2, DEV)
+    got2 = run_fused(dw2, "proj")
+    dw2.release()
+    assert np.array_equal(got2, got[perm])
+
+
+def test_edge_cases():
+    w = random_workload(RANDOM_CASES[2])
+    dw = D.upload(w, DEV)
+    p = dw.projection("proj")
+    x = dw.xs["x"]
+    # empty batch and all-unadapted batch: nothing changes
+    for so, sa in (([0], []), (w.seg_offset, np.full_like(w.seg_adapter, -1))):
+        b = L.Batch(so, sa, n_rows=int(so[-1]))
+        y = p.y.clone()
+        ws = torch.empty(4096, dtype=torch.uint8, device=DEV)
+        L.lora_apply_fused(p.table, b, x, x.shape[1], y, y.shape[1], ws, 4096, stream())
+        torch.cuda.synchronize()
+        assert torch.equal(y, p.y)
+    # a single row
+    b1 = L.Batch([0, 1], [2])
+    y = p.y[:1].clone()
+    ws, n = workspace(p.table, b1)
+    L.lora_apply_fused(p.table, b1, x, x.shape[1], y, y.shape[1], ws, n, stream())
+    torch.cuda.synchronize()
+    ref = oracle.lora_apply([0, 1], [2], w.xs["x"][:1], w.projections[0].A, w.projections[0].B,
+                            w.ranks, w.scales, w.projections[0].y[:1], w.dtype)
+    compare(D.from_device_bits(y), ref, w.dtype, "single row")
+    dw.release()
+
+
+def test_errors_are_reported_not_enqueued():
+    w = random_workload(RANDOM_CASES[0])
+    dw = D.upload(w, DEV)
+    p = dw.projection("proj")
+    x = dw.xs["x"]
+    y = p.y.clone()
+    ws, n = workspace(p.table, dw.batch)
+    with pytest.raises(L.LoraError) as e:
+        L.lora_apply_fused(p.table, dw.batch, x, x.shape[1], y, y.shape[1], ws, n - 1, stream())
+    assert e.value.code == L.LORA_E_WORKSPACE
+    with pytest.raises(L.LoraError) as e:
+        L.lora_apply_fused(p.table, dw.batch, x, x.shape[1], x, x.shape[1], ws, n, stream())
+    assert e.value.code == L.LORA_E_OVERLAP
+    with pytest.raises(L.LoraError) as e:
+        L.lora_apply_fused(p.table, dw.batch, x.data_ptr() + 2, x.shape[1], y, y.shape[1], ws, n,
+                           stream())
+    assert e.value.code == L.LORA_E_ALIGN
+    with pytest.raises(L.LoraError) as e:
+        L.lora_apply_fused(p.table, L.Batch([0, 1], [99]), x, x.shape[1], y, y.shape[1], ws, n,
+                           stream())
+    assert e.value.code == L.LORA_E_INDEX
+    torch.cuda.synchronize()
+    assert torch.equal(y, p.y)
+    dw.release()
+
+
+# ---------------------------------------------------------------------------
+# the named workloads at full size
+# ---------------------------------------------------------------------------
+
+def sampled_rows(w, n_active=12, n_none=2, seed=0):
+    rng = np.random.default_rng(seed)
+    ra = w.row_adapter()
+    act = np.nonzero(ra >= 0)[0]
+    none = np.nonzero(ra < 0)[0]
+    pick = list(rng.choice(act, size=min(n_active, act.size), replace=False))
+    pick += [int(act[0]), int(act[-1])]
+    if none.size:
+        pick += list(rng.choice(none, size=min(n_none, none.size), replace=False))
+    return sorted(set(int(t) for t in pick))
+
+
+@pytest.mark.parametrize("name", list(W.NAMED))
+def test_named_workload_full_size(name):
+    say(f"named workload {name}: generating")
+    w = W.NAMED[name]()
+    dw = D.upload(w, DEV)
+    say(f"  uploaded, T={w.n_rows}")
+    for p in w.projections:
+        got = run_fused(dw, p.name)
+        if w.n_rows <= 64:
+            ref = oracle_full(w, p.name)
+            st = compare(got, ref, w.dtype, f"{name}/{p.name}")
+        else:
+            rows = sampled_rows(w)
+            ref = oracle.lora_apply_rows(rows, w.seg_offset, w.seg_adapter, w.xs[p.x], p.A, p.B,
+                                         w.ranks, w.scales, p.y, w.dtype)
+            st = compare(got[rows], ref, w.dtype, f"{name}/{p.name}")
+        say(f"  {p.name}: {st}")
+        assert np.all(np.isfinite(W.bits_to_f32(got, w.dtype)))
+    dw.release()
