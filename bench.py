@@ -1,0 +1,289 @@
+#!/usr/bin/env python3
+"""Throughput of the batched multi-adapter LoRA delta on one MI355X.
+
+Headline: decode step of 64 tokens on a 4096->4096 projection, 32 adapters of
+ranks {8,16,32,64}, Zipf(1.1) adapter popularity, fp16 (the batched
+heterogeneous-rank decode of Sections 2.3 C2 / 4.1).  One step = one pass of
+the whole delta (plan already resident; shrink then expand) over the step's
+batch; ``value`` is the step's algorithmic HBM bytes per second.  The prompt
+workload (16 segments of U[64,1024] tokens, bf16) is timed the same way and
+reported as tokens/s.
+
+Timing: every step uses the next of R device copies of {adapters, x, y,
+plan}, with R times the footprint above 512 MiB so that neither the 256 MB
+Infinity Cache nor the L2s hold the previous step's data.  Steps are captured
+in HIP graphs (one kernel launch per node, no memset or copy nodes) and
+replayed between HIP events on the capturing stream.  The shrink and the
+expand kernels are also captured alone to give each kernel's average
+duration for the roofline.
+
+Prints exactly one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, datasheet
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16
+METRIC = "LoRA-delta HBM GB/s (% peak) at decode b=64 mixed rank; prefill tokens/s"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--workload", default="decode_mixed")
+    ap.add_argument("--prefill-workload", default="prefill")
+    ap.add_argument("--prefill-steps", type=int, default=40)
+    ap.add_argument("--rotate-mib", type=float, default=640.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    return ap.parse_args()
+
+
+class Rotation:
+    """R device copies of one workload (stand-ins for R layers: their own
+    adapter tables, x and y) sharing one plan per projection, as a serving
+    loop shares the step's plan across all layers."""
+
+    def __init__(self, w, copies, dev, stream):
+        from paper_2401_11240_amd import device as D
+        from paper_2401_11240_amd import lora as L
+        self.L = L
+        self.copies = [D.upload(w, dev, stream=stream) for _ in range(copies)]
+        first = self.copies[0]
+        self.plans = {p.name: L.lora_plan_create(p.table, first.batch, stream) for p in first.projections}
+
+    def step(self, c, stream, phase="apply"):
+        """One pass of the delta over every projection of copy c."""
+        L = self.L
+        dw = self.copies[c]
+        for p in dw.projections:
+            x = dw.xs[p.x]
+            plan = self.plans[p.name]
+            if phase == "apply":
+                L.lora_plan_apply(plan, p.table, x, x.shape[1], p.y, p.y.shape[1], stream)
+            elif phase == "shrink":
+                L.lora_plan_shrink(plan, p.table, x, x.shape[1], stream)
+            elif phase == "expand":
+                L.lora_plan_expand(plan, p.table, p.y, p.y.shape[1], stream)
+
+    def release(self):
+        for h in self.plans.values():
+            self.L.lora_plan_destroy(h)
+        for dw in self.copies:
+            dw.release()
+
+
+def footprint_bytes(w):
+    n = sum(x.nbytes for x in w.xs.values())
+    for p in w.projections:
+        n += sum(a.nbytes for a in p.A) + sum(b.nbytes for b in p.B) + p.y.nbytes
+    return n
+
+
+def time_graph(torch, rot, n_steps, warmup, phase):
+    """Capture one graph of R steps (one per copy) plus a tail graph, replay
+    them so exactly n_steps steps run, and return the elapsed milliseconds."""
+    R = len(rot.copies)
+    s = torch.cuda.Stream()
+    graphs = {}
+    for count in sorted({R, n_steps % R} - {0}):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            for c in range(count):          # eager pass on the capture stream first
+                rot.step(c, s, phase)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=s):
+                for c in range(count):
+                    rot.step(c, s, phase)
+        graphs[count] = g
+    torch.cuda.synchronize()
+    full, tail = divmod(n_steps, R)
+    with torch.cuda.stream(s):
+        for _ in range(max(1, math.ceil(warmup / R))):
+            graphs[R].replay()
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(s)
+        for _ in range(full):
+            graphs[R].replay()
+        if tail:
+            graphs[tail].replay()
+        end.record(s)
+    end.synchronize()
+    torch.cuda.synchronize()
+    return float(start.elapsed_time(end))
+
+
+def measure(torch, w, dev, steps, warmup, rotate_mib, label):
+    from paper_2401_11240_amd import workloads as W
+    fp = footprint_bytes(w)
+    R = max(2, min(256, math.ceil(rotate_mib * 2 ** 20 / fp)))
+    log(f"[{label}] {w.name}: footprint {fp / 2**20:.1f} MiB, {R} rotated copies")
+    s0 = torch.cuda.current_stream(dev)
+    rot = Rotation(w, R, dev, s0)
+    torch.cuda.synchronize()
+    ms = time_graph(torch, rot, steps, warmup, "apply")
+    log(f"[{label}] {steps} steps in {ms:.3f} ms")
+    ms_shrink = time_graph(torch, rot, steps, warmup, "shrink")
+    ms_expand = time_graph(torch, rot, steps, warmup, "expand")
+    log(f"[{label}] shrink-only {ms_shrink:.3f} ms, expand-only {ms_expand:.3f} ms")
+    rot.release()
+    del rot
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    ra = w.row_adapter()
+    used = np.unique(ra[ra >= 0])
+    n_act = int((ra >= 0).sum())
+    e = 2
+    shrink_b = expand_b = 0
+    seen = set()
+    for p in w.projections:
+        shrink_b += sum(int(w.ranks[g]) * p.h_in for g in used) * e
+        if p.x not in seen:
+            seen.add(p.x)
+            shrink_b += n_act * p.h_in * e
+        expand_b += sum(int(w.ranks[g]) * p.h_out for g in used) * e + n_act * 2 * p.h_out * e
+    total_b = W.algorithmic_bytes(w)
+    assert total_b == shrink_b + expand_b
+    flops = W.algorithmic_flops(w)
+    n_proj = len(w.projections)
+    return dict(
+        steps=steps, R=R, ms=ms, ms_per_step=ms / steps, bytes_per_step=total_b,
+        flops_per_step=flops, gbps=total_b * steps / (ms * 1e-3) / 1e9,
+        tokens_per_s=n_act * steps / (ms * 1e-3), n_active=n_act, distinct=int(used.size),
+        shrink=dict(bytes=shrink_b, us=ms_shrink * 1e3 / (steps * n_proj)),
+        expand=dict(bytes=expand_b, us=ms_expand * 1e3 / (steps * n_proj)),
+        n_proj=n_proj,
+    )
+
+
+def cpu_baseline(w, seconds):
+    import oracle
+    from paper_2401_11240_amd import workloads as W
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        for p in w.projections:
+            oracle.lora_apply(w.seg_offset, w.seg_adapter, w.xs[p.x], p.A, p.B, w.ranks, w.scales,
+                              p.y, w.dtype)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    b = W.algorithmic_bytes(w)
+    return dict(value=b * reps / el / 1e9, unit="GB/s", cores=oracle.num_threads(), kind="oracle",
+                sample=f"{reps} full steps of {w.name} (fp64 C oracle, OpenMP over rows), {el:.1f} s",
+                ms_per_step=el * 1e3 / reps)
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus > 1 or world > 1:
+        if int(os.environ.get("RANK", "0")) == 0:
+            log("bench.py measures one GPU only: the delta is data-parallel per GPU and this "
+                "build runs no multi-GPU path; run with --gpus 1.")
+        sys.exit(2)
+
+    import torch
+    from paper_2401_11240_amd import build as B
+    from paper_2401_11240_amd import workloads as W
+    if not os.path.exists(B.lib_path()):
+        B.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    w = W.NAMED[args.workload]()
+    dec = measure(torch, w, dev, args.steps, args.warmup, args.rotate_mib, "decode")
+    dom = "shrink" if dec["shrink"]["us"] >= dec["expand"]["us"] else "expand"
+    dk = dec[dom]
+    achieved = dk["bytes"] / (dk["us"] * 1e-6) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(dec["gbps"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dec["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": W.DTYPE_NAMES[w.dtype],
+        "data": "synthetic (seeded Llama-shaped workload; no datasets or weights)",
+        "config": {
+            "workload": w.name,
+            "h_in": w.projections[0].h_in,
+            "h_out": w.projections[0].h_out,
+            "tokens": w.n_rows,
+            "adapters": w.n_adapters,
+            "distinct_adapters": dec["distinct"],
+            "ranks": sorted(set(int(r) for r in w.ranks)),
+            "adapter_law": "Zipf(1.1)",
+            "rotated_copies": dec["R"],
+            "algorithmic_bytes_per_step": dec["bytes_per_step"],
+            "timing": "HIP graph replays between HIP events",
+            "plan": "one plan per step shared by the rotated layer tables",
+        },
+        "pct_hbm_peak": round(100.0 * dec["gbps"] / HBM_PEAK_GBPS, 2),
+        "roofline": {
+            "kernel": f"lora_{dom}_kernel",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "avg_launch_us": round(dk["us"], 3),
+            "algorithmic_bytes_per_launch": dk["bytes"],
+            "other_kernel": {"name": "lora_" + ("expand" if dom == "shrink" else "shrink") + "_kernel",
+                             "avg_launch_us": round(dec["expand" if dom == "shrink" else "shrink"]["us"], 3),
+                             "algorithmic_bytes_per_launch": dec["expand" if dom == "shrink" else "shrink"]["bytes"]},
+        },
+    }
+    if not args.no_prefill:
+        wp = W.NAMED[args.prefill_workload]()
+        pre = measure(torch, wp, dev, args.prefill_steps, max(4, args.prefill_steps // 10),
+                      args.rotate_mib, "prefill")
+        out["prefill"] = {
+            "workload": wp.name,
+            "tokens_per_s": round(pre["tokens_per_s"], 1),
+            "tokens_per_step": pre["n_active"],
+            "ms_per_step": pre["ms_per_step"],
+            "GBps": round(pre["gbps"], 2),
+            "pct_hbm_peak": round(100.0 * pre["gbps"] / HBM_PEAK_GBPS, 2),
+            "TFLOPs": round(pre["flops_per_step"] / (pre["ms_per_step"] * 1e-3) / 1e12, 3),
+            "shrink_us": round(pre["shrink"]["us"], 2),
+            "expand_us": round(pre["expand"]["us"], 2),
+            "algorithmic_bytes_per_step": pre["bytes_per_step"],
+            "rotated_copies": pre["R"],
+        }
+    if not args.no_cpu_baseline:
+        log("[cpu] timing the oracle")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -134,27 +134,35 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
                      int64_t ldy, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Plan a batch once and apply it many times (the same step's batch applies to
- * every adapted projection of every layer).  lora_plan_create validates the
- * batch, builds the rank-bucketed work list on the host and uploads it, with
- * its own workspace, to device memory owned by the plan (allocates; not for
- * the hot loop).  lora_plan_apply is lora_apply_fused without the upload: it
- * enqueues kernels only.  Calls on one plan must be ordered (one stream).
+ * Plan a batch once and apply it many times: the batch of a step is the same
+ * for every adapted projection of every layer, so the grouping and the work
+ * list are built once.  lora_plan_create validates the batch, builds the
+ * rank-bucketed work list on the host from table t's ranks and shapes and
+ * uploads it, with its own workspace, to device memory owned by the plan
+ * (allocates; not for the hot loop).
+ *
+ * lora_plan_apply runs the whole delta (lora_apply_fused without the upload:
+ * it enqueues kernels only) with the adapters of table t, or of the table the
+ * plan was made with when t is NULL.  Any table with the same h_in, h_out and
+ * dtype whose adapters referenced by the batch have the same ranks may be
+ * used (e.g. the same adapters' factors in another layer); the weight
+ * pointers and scales travel in the launch arguments.  A mismatch returns
+ * LORA_E_SHAPE / LORA_E_RANK / LORA_E_INDEX and enqueues nothing.
+ *
+ * lora_plan_shrink and lora_plan_expand are the two halves as separate
+ * launches (one kernel each), for callers that schedule or time them apart:
+ * the shrink writes the float32 partial results of x.A_g into the plan's
+ * workspace, the expand adds s_g * v.B_g into y from there.  An expand must
+ * follow a shrink of the same plan in stream order; the pair computes exactly
+ * what lora_plan_apply computes.  Calls on one plan must be ordered (one
+ * stream): they share its workspace.
  */
 int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream);
-int lora_plan_apply(lora_plan_t p, const void* x, int64_t ldx, void* y, int64_t ldy, void* stream);
+int lora_plan_apply(lora_plan_t p, lora_table_t t, const void* x, int64_t ldx, void* y,
+                    int64_t ldy, void* stream);
+int lora_plan_shrink(lora_plan_t p, lora_table_t t, const void* x, int64_t ldx, void* stream);
+int lora_plan_expand(lora_plan_t p, lora_table_t t, void* y, int64_t ldy, void* stream);
 int lora_plan_destroy(lora_plan_t p);
-
-/*
- * The two halves of lora_plan_apply as separate launches (one kernel each),
- * for callers that schedule them apart or time them one by one:
- * lora_plan_shrink writes the float32 intermediate x.A_g into the plan's own
- * workspace; lora_plan_expand adds s_g * v.B_g into y from that workspace.
- * lora_plan_expand must follow a lora_plan_shrink of the same plan in stream
- * order; the pair computes exactly what lora_plan_apply computes.
- */
-int lora_plan_shrink(lora_plan_t p, const void* x, int64_t ldx, void* stream);
-int lora_plan_expand(lora_plan_t p, void* y, int64_t ldy, void* stream);
 
 /*
  * The integer part of the plan, on the host only (no GPU needed): rows that

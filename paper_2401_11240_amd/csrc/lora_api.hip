@@ -2,10 +2,11 @@
 // argument validation, the rank-bucketed planner and the launches.
 //
 // Everything a call needs is checked here before anything is enqueued, so a
-// bad argument never reaches a kernel.  The planner turns the step's
-// segments into (a) the rows grouped by adapter and (b) a flat list of work
-// items sized by bytes, then the plan is copied into the caller's workspace
-// in stream order and the kernels read it from there.
+// bad argument never reaches a kernel.  The planner turns the step's segments
+// into (a) the rows grouped by adapter and (b) flat lists of work items sized
+// by bytes.  A plan depends on the batch, the ranks and the shapes only; each
+// launch carries the weight pointers and scales of the table it is applied
+// to, so one plan serves every compatible table.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -22,6 +23,7 @@
 namespace lora {
 hipError_t launch_shrink(const KernelArgs& a, int dtype, hipStream_t s);
 hipError_t launch_expand(const KernelArgs& a, int dtype, hipStream_t s);
+hipError_t launch_reduce(const KernelArgs& a, hipStream_t s);
 }  // namespace lora
 
 using namespace lora;
@@ -46,23 +48,9 @@ constexpr size_t kAlign = 256;
 inline size_t align_up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-bool fast_rank(int r) {
-    return r == 8 || r == 16 || r == 32 || r == 64 || r == 128 || r == 256;
-}
-
-// Rows of A_g per shrink item and columns of B_g per expand item.  Fast
-// ranks move kChunkElems elements per item; other ranks use a smaller chunk
-// so the generic body's LDS staging fits.
-int shrink_klen(int r) {
-    if (fast_rank(r)) return kChunkElems / r;
-    int k = (8192 / r) & ~7;
-    return std::max(8, k);
-}
-int expand_nlen(int r) {
-    if (fast_rank(r)) return kChunkElems / r;
-    int n = (kChunkElems / r) & ~7;
-    return std::max(8, n);
-}
+// Workgroups the planner aims for when it sizes the K ranges of prompt-sized
+// row blocks (two per CU on a 256-CU device).
+constexpr int kTargetItems = 512;
 
 struct DeviceGuard {
     int prev = -1;
@@ -95,16 +83,15 @@ struct lora_table_s {
 namespace {
 
 struct HostPlan {
+    int h_in = 0, h_out = 0, dtype = 0, n_adapters = 0;
     int n_active = 0;
     int n_groups = 0;
     int r_max = 0;
-    int vld = 0;
-    std::vector<int32_t> perm, group_off, group_adapter;
-    std::vector<DevItem> shrink, expand;
-    std::vector<int64_t> part_off;
+    std::vector<int32_t> perm, group_off, group_adapter, group_rank;
+    std::vector<DevItem> shrink, expand, reduce;
     int64_t n_partials = 0;
-    size_t off_shrink = 0, off_expand = 0, off_perm = 0, off_partoff = 0, off_counters = 0;
-    size_t plan_bytes = 0, off_v = 0, off_partials = 0, total_bytes = 0;
+    size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_perm = 0;
+    size_t plan_bytes = 0, off_partials = 0, total_bytes = 0;
     std::vector<unsigned char> blob;
 };
 
@@ -162,81 +149,129 @@ void group_rows(const lora_batch_t* b, int n_adapters, std::vector<int32_t>& per
 int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     int rc = validate_batch(b, t->n);
     if (rc) return rc;
+    p.h_in = t->h_in;
+    p.h_out = t->h_out;
+    p.dtype = t->dtype;
+    p.n_adapters = t->n;
     group_rows(b, t->n, p.perm, p.group_off, p.group_adapter);
     p.n_groups = (int)p.group_adapter.size();
     p.n_active = p.n_groups ? p.group_off[p.n_groups] : 0;
+    p.group_rank.assign(p.n_groups, 0);
     p.r_max = 0;
     p.shrink.clear();
     p.expand.clear();
-    p.part_off.assign(p.n_groups, 0);
+    p.reduce.clear();
     p.n_partials = 0;
+
+    // Prompt-sized row blocks (more than 16 rows) stream their K range in
+    // several passes; how many K ranges they are cut into follows from how
+    // many such blocks the batch has.
+    int big_blocks = 0;
     for (int g = 0; g < p.n_groups; ++g) {
-        const int a = p.group_adapter[g];
-        const int r = t->host[a].rank;
+        const int r = t->host[p.group_adapter[g]].rank;
+        const int rb = row_block(r);
         const int n = p.group_off[g + 1] - p.group_off[g];
-        const int p0 = p.group_off[g];
+        for (int q0 = 0; q0 < n; q0 += rb)
+            if (std::min(rb, n - q0) > kInlineRows) ++big_blocks;
+    }
+    const int big_split = big_blocks ? std::max(1, std::min(8, (kTargetItems + big_blocks - 1) / big_blocks)) : 1;
+
+    for (int g = 0; g < p.n_groups; ++g) {
+        const DevAdapter& ad = t->host[p.group_adapter[g]];
+        const int r = ad.rank;
+        p.group_rank[g] = r;
         p.r_max = std::max(p.r_max, r);
-        const int klen = shrink_klen(r);
-        const int nsplit = (t->h_in + klen - 1) / klen;
-        if (nsplit > 0xffff) return fail(LORA_E_SHAPE, "h_in too large for the chunking");
-        for (int c = 0; c < nsplit; ++c) {
-            DevItem it{};
-            it.kind = kItemShrink;
-            it.adapter = a;
-            it.p0 = p0;
-            it.nrows = n;
-            it.lo = c * klen;
-            it.len = std::min(klen, t->h_in - c * klen);
-            it.group = g;
-            it.split = (c << 16) | nsplit;
-            p.shrink.push_back(it);
-        }
-        p.part_off[g] = p.n_partials;
-        if (nsplit > 1) p.n_partials += (int64_t)nsplit * n * r;
-        const int nlen = expand_nlen(r);
-        const int ntiles = (t->h_out + nlen - 1) / nlen;
-        for (int c = 0; c < ntiles; ++c) {
-            DevItem it{};
-            it.kind = kItemExpand;
-            it.adapter = a;
-            it.p0 = p0;
-            it.nrows = n;
-            it.lo = c * nlen;
-            it.len = std::min(nlen, t->h_out - c * nlen);
-            it.group = g;
-            it.split = 0;
-            p.expand.push_back(it);
+        const int rb = row_block(r);
+        for (int p0 = p.group_off[g]; p0 < p.group_off[g + 1]; p0 += rb) {
+            const int nb = std::min(rb, p.group_off[g + 1] - p0);
+            const int sub = shrink_sub(r, nb);
+            int krange = sub;
+            if (nb > kInlineRows) {
+                const int per = (t->h_in + big_split - 1) / big_split;
+                krange = round_up_i(std::max(per, sub), sub);
+            }
+            const int nsplit = (t->h_in + krange - 1) / krange;
+            const int pstride = round_up_i(nb * r, 4);
+            const int nlen = expand_nlen(r, nb);
+            const int ntiles = (t->h_out + nlen - 1) / nlen;
+            DevItem base{};
+            base.group = g;
+            base.adapter = p.group_adapter[g];
+            base.rank = r;
+            base.nrows = nb;
+            base.nsplit = nsplit;
+            base.p0 = p0;
+            base.pstride = pstride;
+            if (nb <= kInlineRows)
+                for (int i = 0; i < nb; ++i) base.rows[i] = p.perm[p0 + i];
+            const int64_t part0 = p.n_partials;
+            p.n_partials += (int64_t)nsplit * pstride;
+            for (int c = 0; c < nsplit; ++c) {
+                DevItem it = base;
+                it.kind = kItemShrink;
+                it.part = part0 + (int64_t)c * pstride;
+                it.lo = c * krange;
+                it.len = std::min(krange, t->h_in - c * krange);
+                it.sub = sub;
+                if (shrink_lds_bytes(r, sub, nb) > kShrinkLds)
+                    return fail(LORA_E_SHAPE, "internal: shrink tile exceeds LDS");
+                p.shrink.push_back(it);
+            }
+            for (int c = 0; c < ntiles; ++c) {
+                DevItem it = base;
+                it.kind = kItemExpand;
+                it.part = part0;
+                it.lo = c * nlen;
+                it.len = std::min(nlen, t->h_out - c * nlen);
+                if (expand_lds_bytes(r, it.len, nb) > kExpandLds)
+                    return fail(LORA_E_SHAPE, "internal: expand tile exceeds LDS");
+                p.expand.push_back(it);
+            }
+            DevItem it = base;
+            it.kind = kItemReduce;
+            it.part = part0;
+            p.reduce.push_back(it);
         }
     }
-    p.vld = std::max(4, (p.r_max + 3) / 4 * 4);
 
-    // device layout: [shrink items][expand items][perm][part_off][counters] | [v][partials]
+    // device layout: [shrink items][expand items][reduce items][perm] | [partials]
     size_t off = 0;
     p.off_shrink = off;
     off = align_up(off + p.shrink.size() * sizeof(DevItem));
     p.off_expand = off;
     off = align_up(off + p.expand.size() * sizeof(DevItem));
+    p.off_reduce = off;
+    off = align_up(off + p.reduce.size() * sizeof(DevItem));
     p.off_perm = off;
     off = align_up(off + p.perm.size() * sizeof(int32_t));
-    p.off_partoff = off;
-    off = align_up(off + p.part_off.size() * sizeof(int64_t));
-    p.off_counters = off;
-    off = align_up(off + (size_t)p.n_groups * sizeof(int32_t));
     p.plan_bytes = off;
-    p.off_v = off;
-    off = align_up(off + (size_t)p.n_active * p.vld * sizeof(float));
     p.off_partials = off;
     off = align_up(off + (size_t)p.n_partials * sizeof(float));
     p.total_bytes = std::max<size_t>(off, kAlign);
 
-    p.blob.assign(p.plan_bytes, 0);   // counters start at zero
+    p.blob.assign(p.plan_bytes, 0);
     auto put = [&](size_t at, const void* src, size_t n) {
         if (n) std::memcpy(p.blob.data() + at, src, n);
     };
     put(p.off_shrink, p.shrink.data(), p.shrink.size() * sizeof(DevItem));
     put(p.off_expand, p.expand.data(), p.expand.size() * sizeof(DevItem));
+    put(p.off_reduce, p.reduce.data(), p.reduce.size() * sizeof(DevItem));
     put(p.off_perm, p.perm.data(), p.perm.size() * sizeof(int32_t));
-    put(p.off_partoff, p.part_off.data(), p.part_off.size() * sizeof(int64_t));
+    return LORA_OK;
+}
+
+// A table may run a plan made with another table when shapes, dtype and the
+// ranks of every adapter the plan references agree.
+int check_compatible(const HostPlan& p, const lora_table_s* t) {
+    if (!t || !t->dev) return fail(LORA_E_ARG, "table is NULL or released");
+    if (t->h_in != p.h_in || t->h_out != p.h_out || t->dtype != p.dtype)
+        return fail(LORA_E_SHAPE, "table shape or dtype differs from the plan's");
+    for (int g = 0; g < p.n_groups; ++g) {
+        const int a = p.group_adapter[g];
+        if (a >= t->n) return fail(LORA_E_INDEX, "table has fewer adapters than the plan references");
+        if (t->host[a].rank != p.group_rank[g])
+            return fail(LORA_E_RANK, "adapter " + std::to_string(a) + " has another rank than in the plan");
+    }
     return LORA_OK;
 }
 
@@ -284,15 +319,22 @@ int stage_upload(int device, const void* src, size_t bytes, void* dst, hipStream
     return LORA_OK;
 }
 
-KernelArgs base_args(const lora_table_s* t, const HostPlan& p, unsigned char* ws) {
+// Launch arguments of one plan on one table: the plan's buffers in workspace
+// w, and the group pointer table of the shrink (A) or expand (B) factors.
+KernelArgs make_args(const lora_table_s* t, const HostPlan& p, unsigned char* w, bool shrink_side) {
     KernelArgs a{};
+    a.perm = (const int32_t*)(w + p.off_perm);
     a.table = t->dev;
-    a.perm = (const int32_t*)(ws + p.off_perm);
-    a.counters = (int32_t*)(ws + p.off_counters);
-    a.partials = (float*)(ws + p.off_partials);
-    a.part_off = (const int64_t*)(ws + p.off_partoff);
+    a.partials = (float*)(w + p.off_partials);
     a.h_in = t->h_in;
     a.h_out = t->h_out;
+    a.n_groups = p.n_groups;
+    const int ng = std::min(p.n_groups, kKargGroups);
+    for (int g = 0; g < ng; ++g) {
+        const DevAdapter& ad = t->host[p.group_adapter[g]];
+        a.gptr[g] = shrink_side ? ad.A : ad.B;
+        a.gscale[g] = ad.scale;
+    }
     return a;
 }
 
@@ -324,6 +366,49 @@ int check_ws(const HostPlan& p, const void* ws, size_t ws_bytes) {
     if (ws_bytes < p.total_bytes)
         return fail(LORA_E_WORKSPACE, "workspace has " + std::to_string(ws_bytes) +
                                           " bytes, needs " + std::to_string(p.total_bytes));
+    return LORA_OK;
+}
+
+int check_x(const lora_table_s* t, const void* x, int64_t ldx) {
+    if (!x) return fail(LORA_E_ARG, "x is NULL");
+    if (!aligned16(x)) return fail(LORA_E_ALIGN, "x not 16-byte aligned");
+    return check_ld("ldx", ldx, t->h_in);
+}
+
+int check_y(const lora_table_s* t, const void* y, int64_t ldy) {
+    if (!y) return fail(LORA_E_ARG, "y is NULL");
+    if (!aligned16(y)) return fail(LORA_E_ALIGN, "y not 16-byte aligned");
+    return check_ld("ldy", ldy, t->h_out);
+}
+
+int check_v(const HostPlan& p, const void* v, int64_t ldv) {
+    if (!v) return fail(LORA_E_ARG, "v is NULL");
+    if (!aligned16(v)) return fail(LORA_E_ALIGN, "v not 16-byte aligned");
+    if (ldv < p.r_max || ldv % 4)
+        return fail(LORA_E_SHAPE, "ldv must be a multiple of 4 and >= the largest rank used");
+    return LORA_OK;
+}
+
+// Enqueue the shrink (x != NULL) and/or the expand (y != NULL) of plan p on
+// table t with its workspace at w.
+int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x, int64_t ldx,
+            void* y, int64_t ldy, hipStream_t s) {
+    if (x) {
+        KernelArgs a = make_args(t, p, w, true);
+        a.items = (const DevItem*)(w + p.off_shrink);
+        a.n_items = (int32_t)p.shrink.size();
+        a.x = x;
+        a.ldx = ldx;
+        LORA_HIP_TRY(launch_shrink(a, t->dtype, s));
+    }
+    if (y) {
+        KernelArgs a = make_args(t, p, w, false);
+        a.items = (const DevItem*)(w + p.off_expand);
+        a.n_items = (int32_t)p.expand.size();
+        a.y = y;
+        a.ldy = ldy;
+        LORA_HIP_TRY(launch_expand(a, t->dtype, s));
+    }
     return LORA_OK;
 }
 
@@ -444,24 +529,20 @@ int lora_shrink(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ld
     HostPlan p;
     if (int rc = build_plan(t, b, p)) return rc;
     if (p.n_active == 0) return LORA_OK;
-    if (!x || !v) return fail(LORA_E_ARG, "x or v is NULL");
-    if (!aligned16(x) || !aligned16(v)) return fail(LORA_E_ALIGN, "x or v not 16-byte aligned");
-    if (int rc = check_ld("ldx", ldx, t->h_in)) return rc;
-    if (ldv < p.r_max || ldv % 4) return fail(LORA_E_SHAPE, "ldv must be a multiple of 4 and >= the largest rank used");
+    if (int rc = check_x(t, x, ldx)) return rc;
+    if (int rc = check_v(p, v, ldv)) return rc;
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
-    KernelArgs a = base_args(t, p, w);
-    a.items = (const DevItem*)(w + p.off_shrink);
-    a.n_items = (int32_t)p.shrink.size();
-    a.x = x;
-    a.ldx = ldx;
+    if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s)) return rc;
+    KernelArgs a = make_args(t, p, w, true);
+    a.items = (const DevItem*)(w + p.off_reduce);
+    a.n_items = (int32_t)p.reduce.size();
     a.v = v;
     a.ldv = ldv;
-    a.v_by_row = 1;
-    LORA_HIP_TRY(launch_shrink(a, t->dtype, s));
+    LORA_HIP_TRY(launch_reduce(a, s));
     return LORA_OK;
 }
 
@@ -471,59 +552,22 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
     HostPlan p;
     if (int rc = build_plan(t, b, p)) return rc;
     if (p.n_active == 0) return LORA_OK;
-    if (!v || !y) return fail(LORA_E_ARG, "v or y is NULL");
-    if (!aligned16(v) || !aligned16(y)) return fail(LORA_E_ALIGN, "v or y not 16-byte aligned");
-    if (int rc = check_ld("ldy", ldy, t->h_out)) return rc;
-    if (ldv < p.r_max || ldv % 4) return fail(LORA_E_SHAPE, "ldv must be a multiple of 4 and >= the largest rank used");
+    if (int rc = check_v(p, v, ldv)) return rc;
+    if (int rc = check_y(t, y, ldy)) return rc;
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
-    KernelArgs a = base_args(t, p, w);
+    KernelArgs a = make_args(t, p, w, false);
     a.items = (const DevItem*)(w + p.off_expand);
     a.n_items = (int32_t)p.expand.size();
     a.v = const_cast<float*>(v);
     a.ldv = ldv;
-    a.v_by_row = 1;
     a.y = y;
     a.ldy = ldy;
     LORA_HIP_TRY(launch_expand(a, t->dtype, s));
     return LORA_OK;
-}
-
-// Launch the shrink (x != NULL) and/or the expand (y != NULL) of a plan whose
-// float32 intermediate lives in the workspace w.
-static int enqueue_apply(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x,
-                         int64_t ldx, void* y, int64_t ldy, hipStream_t s) {
-    KernelArgs a = base_args(t, p, w);
-    a.x = x;
-    a.ldx = ldx;
-    a.v = (float*)(w + p.off_v);
-    a.ldv = p.vld;
-    a.v_by_row = 0;
-    a.y = y;
-    a.ldy = ldy;
-    if (x) {
-        a.items = (const DevItem*)(w + p.off_shrink);
-        a.n_items = (int32_t)p.shrink.size();
-        LORA_HIP_TRY(launch_shrink(a, t->dtype, s));
-    }
-    if (y) {
-        a.items = (const DevItem*)(w + p.off_expand);
-        a.n_items = (int32_t)p.expand.size();
-        LORA_HIP_TRY(launch_expand(a, t->dtype, s));
-    }
-    return LORA_OK;
-}
-
-static int check_xy(const lora_table_s* t, int n_rows, const void* x, int64_t ldx, const void* y,
-                    int64_t ldy) {
-    if (!x || !y) return fail(LORA_E_ARG, "x or y is NULL");
-    if (!aligned16(x) || !aligned16(y)) return fail(LORA_E_ALIGN, "x or y not 16-byte aligned");
-    if (int rc = check_ld("ldx", ldx, t->h_in)) return rc;
-    if (int rc = check_ld("ldy", ldy, t->h_out)) return rc;
-    return check_overlap(x, ldx, t->h_in, y, ldy, t->h_out, n_rows);
 }
 
 int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,
@@ -532,13 +576,15 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
     HostPlan p;
     if (int rc = build_plan(t, b, p)) return rc;
     if (p.n_active == 0) return LORA_OK;
-    if (int rc = check_xy(t, b->n_rows, x, ldx, y, ldy)) return rc;
+    if (int rc = check_x(t, x, ldx)) return rc;
+    if (int rc = check_y(t, y, ldy)) return rc;
+    if (int rc = check_overlap(x, ldx, t->h_in, y, ldy, t->h_out, b->n_rows)) return rc;
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
-    return enqueue_apply(t, p, w, x, ldx, y, ldy, s);
+    return enqueue(t, p, w, x, ldx, y, ldy, s);
 }
 
 int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream) {
@@ -548,11 +594,11 @@ int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, vo
     auto* pl = new (std::nothrow) lora_plan_s();
     if (!pl) return fail(LORA_E_NOMEM, "plan allocation failed");
     pl->table = t;
-    pl->n_rows = b ? b->n_rows : 0;
     if (int rc = build_plan(t, b, pl->plan)) {
         delete pl;
         return rc;
     }
+    pl->n_rows = b->n_rows;
     DeviceGuard dg(t->device);
     hipError_t e = hipMalloc((void**)&pl->dmem, pl->plan.total_bytes);
     if (e != hipSuccess) {
@@ -571,35 +617,36 @@ int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, vo
     return LORA_OK;
 }
 
-int lora_plan_apply(lora_plan_t pl, const void* x, int64_t ldx, void* y, int64_t ldy, void* stream) {
+static int plan_run(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, void* y, int64_t ldy,
+                    void* stream) {
     if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
-    const lora_table_s* t = pl->table;
+    const lora_table_s* tt = t ? t : pl->table;
+    if (int rc = check_compatible(pl->plan, tt)) return rc;
     if (pl->plan.n_active == 0) return LORA_OK;
-    if (int rc = check_xy(t, pl->n_rows, x, ldx, y, ldy)) return rc;
-    DeviceGuard dg(t->device);
-    return enqueue_apply(t, pl->plan, pl->dmem, x, ldx, y, ldy, (hipStream_t)stream);
+    if (x)
+        if (int rc = check_x(tt, x, ldx)) return rc;
+    if (y)
+        if (int rc = check_y(tt, y, ldy)) return rc;
+    if (x && y)
+        if (int rc = check_overlap(x, ldx, tt->h_in, y, ldy, tt->h_out, pl->n_rows)) return rc;
+    DeviceGuard dg(tt->device);
+    return enqueue(tt, pl->plan, pl->dmem, x, ldx, y, ldy, (hipStream_t)stream);
 }
 
-int lora_plan_shrink(lora_plan_t pl, const void* x, int64_t ldx, void* stream) {
-    if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
-    const lora_table_s* t = pl->table;
-    if (pl->plan.n_active == 0) return LORA_OK;
+int lora_plan_apply(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, void* y, int64_t ldy,
+                    void* stream) {
+    if (!x || !y) return fail(LORA_E_ARG, "x or y is NULL");
+    return plan_run(pl, t, x, ldx, y, ldy, stream);
+}
+
+int lora_plan_shrink(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, void* stream) {
     if (!x) return fail(LORA_E_ARG, "x is NULL");
-    if (!aligned16(x)) return fail(LORA_E_ALIGN, "x not 16-byte aligned");
-    if (int rc = check_ld("ldx", ldx, t->h_in)) return rc;
-    DeviceGuard dg(t->device);
-    return enqueue_apply(t, pl->plan, pl->dmem, x, ldx, nullptr, 0, (hipStream_t)stream);
+    return plan_run(pl, t, x, ldx, nullptr, 0, stream);
 }
 
-int lora_plan_expand(lora_plan_t pl, void* y, int64_t ldy, void* stream) {
-    if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
-    const lora_table_s* t = pl->table;
-    if (pl->plan.n_active == 0) return LORA_OK;
+int lora_plan_expand(lora_plan_t pl, lora_table_t t, void* y, int64_t ldy, void* stream) {
     if (!y) return fail(LORA_E_ARG, "y is NULL");
-    if (!aligned16(y)) return fail(LORA_E_ALIGN, "y not 16-byte aligned");
-    if (int rc = check_ld("ldy", ldy, t->h_out)) return rc;
-    DeviceGuard dg(t->device);
-    return enqueue_apply(t, pl->plan, pl->dmem, nullptr, 0, y, ldy, (hipStream_t)stream);
+    return plan_run(pl, t, nullptr, 0, y, ldy, stream);
 }
 
 int lora_plan_destroy(lora_plan_t pl) {

@@ -1,36 +1,56 @@
 // gfx950 kernels of the batched, heterogeneous-rank LoRA delta
 //   y[t,:] <- round(y[t,:] + s_g * (x[t,:] . A_g) . B_g)          (Eq. 1)
 //
-// Shrink: one workgroup per (adapter group, K-chunk of A_g).  The chunk of
-// A_g (rows k0..k0+klen of the row-major [h_in, r] matrix) is one contiguous
-// run of bytes, streamed once per step with 16-byte loads, whatever the
-// number of tokens that use the adapter: tokens are gathered to their adapter
-// instead of each token re-reading its adapter (the gather of Section 4.1
-// done once per distinct adapter).  The group's x rows for the chunk sit in
-// LDS; products accumulate in float32; lanes that share an output column
-// reduce with cross-lane shuffles, then across the four waves through LDS in
-// a fixed order.  When a group's h_in is split over several workgroups, each
-// writes its partial sums; the last to arrive (atomic counter) adds them in
-// chunk order, so results never depend on timing.
+// Shrink: one workgroup per (row block of an adapter group, K range of A_g).
+// A's rows k0..k0+len are one contiguous run of bytes, read once per step
+// with 16-byte loads however many tokens use the adapter: tokens are gathered
+// to their adapter instead of each token re-reading it (Section 4.1's gather,
+// done once per distinct adapter).  The range is staged in passes: A goes to
+// LDS transposed into words that hold two consecutive K elements of one rank,
+// the row block's x columns go to LDS as they are, and the next pass's loads
+// are in flight while the current pass runs on v_mfma_f32_16x16x32
+// (v^T[r, t] = sum_k A[k, r] x[t, k], 16 ranks x 16 rows x 32 K per
+// instruction, float32 accumulation).  When a rank has fewer tiles than waves,
+// the waves split K and add their sums through LDS in wave order.  The
+// workgroup writes its float32 partial block.
 //
-// Expand: one workgroup per (adapter group, column tile of B_g).  Each lane
-// owns 8 consecutive output columns (16-byte loads and stores of B and y) and
-// 8 consecutive ranks; the float32 intermediate v of the group's rows is read
-// from LDS; partial sums over rank slices are added in a fixed order and
-// y + s*d is rounded once to the storage dtype.
+// Expand: one workgroup per (row block, column tile of B_g).  It adds the row
+// block's partial blocks in a fixed order (v stays float32 up to here),
+// splits each v into a high and a low 16-bit part so that v is never rounded
+// to one 16-bit value, stages the B tile in LDS transposed into rank pairs and
+// runs y^T[n, t] = sum_j B[j, n] v[t, j] on v_mfma_f32_16x16x16 (two
+// instructions per step: high and low part).  Each lane then holds four
+// consecutive columns of one row of y; y + s*d is rounded once to the storage
+// dtype and written with 8-byte stores.  The B tile, the y values and the
+// partial blocks are all requested before the first barrier.
 //
-// Ranks 8, 16, 32, 64, 128 and 256 have compile-time specialised bodies;
-// any other rank in [1, 256] takes a generic body.  All of them are
-// selected per workgroup inside one grid, so items of different ranks run
-// concurrently instead of queueing behind each other.
+// Rank is a runtime value: any rank in [1, 256] runs the same code (padded to
+// a multiple of 16 inside LDS and registers only), so items of different
+// ranks share one grid; the bodies are compiled for the number of rank tiles
+// (or column tiles) per wave and of 16-row subtiles, so the MFMA loops have no
+// branches.  No workgroup waits for another: results are independent of
+// scheduling and bit-reproducible.
 #include <hip/hip_runtime.h>
 
 #include "lora_internal.h"
 
 namespace lora {
 
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+// Native vectors (not HIP's struct vector types): selects stay in registers.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+// Adapter factors are reached through pointers read at run time; they are
+// global memory, said explicitly so that the loads are global, not flat.
+typedef __attribute__((address_space(1))) const uint16_t gu16;
+typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+
 // ---------------------------------------------------------------------------
-// 16-bit storage formats
+// 16-bit storage formats and their MFMA instructions
 // ---------------------------------------------------------------------------
 struct FmtF16 {
     static __device__ __forceinline__ float to_f32(uint32_t b16) {
@@ -39,439 +59,543 @@ struct FmtF16 {
     static __device__ __forceinline__ uint32_t from_f32(float f) {
         return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
     }
+    static __device__ __forceinline__ f32x4 mma32(const u32x4& a, const u32x4& b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                      __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ f32x4 mma16(const u32x2& a, const u32x2& b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a),
+                                                     __builtin_bit_cast(f16x4, b), c, 0, 0, 0);
+    }
 };
 struct FmtBF16 {
-    static __device__ __forceinline__ float to_f32(uint32_t b16) {
-        return __uint_as_float(b16 << 16);
-    }
+    static __device__ __forceinline__ float to_f32(uint32_t b16) { return __uint_as_float(b16 << 16); }
     static __device__ __forceinline__ uint32_t from_f32(float f) {
         return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
     }
+    static __device__ __forceinline__ f32x4 mma32(const u32x4& a, const u32x4& b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ f32x4 mma16(const u32x2& a, const u32x2& b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a),
+                                                         __builtin_bit_cast(i16x4, b), c, 0, 0, 0);
+    }
 };
 
-template <class Fmt>
-__device__ __forceinline__ void unpack8(const uint4& v, float f[8]) {
-    f[0] = Fmt::to_f32(v.x & 0xffffu); f[1] = Fmt::to_f32(v.x >> 16);
-    f[2] = Fmt::to_f32(v.y & 0xffffu); f[3] = Fmt::to_f32(v.y >> 16);
-    f[4] = Fmt::to_f32(v.z & 0xffffu); f[5] = Fmt::to_f32(v.z >> 16);
-    f[6] = Fmt::to_f32(v.w & 0xffffu); f[7] = Fmt::to_f32(v.w >> 16);
+// The work item, field by field in scalar registers (the whole struct is
+// never copied as one aggregate, which would send it to scratch memory).
+struct Item {
+    int64_t part;
+    int kind, group, adapter, rank, nrows, lo, len, sub, nsplit, p0, pstride;
+    int rows[kInlineRows];
+};
+
+__device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
+    Item it;
+    it.part = p->part;
+    it.kind = p->kind;
+    it.group = p->group;
+    it.adapter = p->adapter;
+    it.rank = p->rank;
+    it.nrows = p->nrows;
+    it.lo = p->lo;
+    it.len = p->len;
+    it.sub = p->sub;
+    it.nsplit = p->nsplit;
+    it.p0 = p->p0;
+    it.pstride = p->pstride;
+#pragma unroll
+    for (int q = 0; q < kInlineRows; ++q) it.rows[q] = p->rows[q];
+    return it;
 }
 
-template <class Fmt>
-__device__ __forceinline__ uint4 pack8(const float f[8]) {
-    uint4 v;
-    v.x = Fmt::from_f32(f[0]) | (Fmt::from_f32(f[1]) << 16);
-    v.y = Fmt::from_f32(f[2]) | (Fmt::from_f32(f[3]) << 16);
-    v.z = Fmt::from_f32(f[4]) | (Fmt::from_f32(f[5]) << 16);
-    v.w = Fmt::from_f32(f[6]) | (Fmt::from_f32(f[7]) << 16);
+__device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xffffu; }
+__device__ __forceinline__ uint32_t hi16(uint32_t w) { return w >> 16; }
+
+// The factor this item streams and the group's scale: from the launch's
+// argument table, or from the device registry for groups beyond it.
+__device__ __forceinline__ gu16* item_factor(const KernelArgs& a, const Item& it, bool shrink) {
+    if (it.group < kKargGroups) return (gu16*)a.gptr[it.group];
+    const DevAdapter* d = a.table + it.adapter;
+    return (gu16*)(shrink ? d->A : d->B);
+}
+__device__ __forceinline__ float item_scale(const KernelArgs& a, const Item& it) {
+    if (it.group < kKargGroups) return a.gscale[it.group];
+    return a.table[it.adapter].scale;
+}
+
+// v with lane Q replaced by the wave-uniform value s (one VALU lane write).
+template <int Q>
+__device__ __forceinline__ int write_lane(int v, int s) {
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(s), "n"(Q));
+    return v;
+}
+template <int Q>
+__device__ __forceinline__ int write_rows(int v, const Item& it) {
+    if constexpr (Q < kInlineRows) return write_rows<Q + 1>(write_lane<Q>(v, it.rows[Q]), it);
     return v;
 }
 
-__device__ __forceinline__ int64_t v_row(const KernelArgs& a, int p) {
-    return a.v_by_row ? (int64_t)a.perm[p] : (int64_t)p;
+// Lane l of every wave holds the item's row l (nrows <= 64): built from the
+// inline rows with lane writes, or read from the grouped row order.  Must be
+// called with every lane active.
+__device__ __forceinline__ int lane_rows(const KernelArgs& a, const Item& it) {
+    if (it.nrows <= kInlineRows) return write_rows<0>(0, it);
+    const int lane = threadIdx.x & 63;
+    return lane < it.nrows ? a.perm[it.p0 + lane] : 0;
+}
+// The item's r-th row, fetched from lane r (every lane active).
+__device__ __forceinline__ int row_of(int rowv, int r) {
+    return __builtin_amdgcn_ds_bpermute(r << 2, rowv);
 }
 
-// Where the shrink result of (group-local row i, rank j) goes: the final v
-// when the group's h_in is a single chunk, else this chunk's partial slot.
-__device__ __forceinline__ void shrink_store(const KernelArgs& a, const DevItem& it, int R, int i,
-                                             int j, float s) {
-    const int nsplit = it.split & 0xffff;
-    if (nsplit == 1) {
-        a.v[v_row(a, it.p0 + i) * a.ldv + j] = s;
-    } else {
-        const int chunk = it.split >> 16;
-        a.partials[a.part_off[it.group] + ((int64_t)chunk * it.nrows + i) * R + j] = s;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Shrink, rank R in {8,16,32,64,128,256}
-// ---------------------------------------------------------------------------
-constexpr int kShrinkLdsBytes = 32768;
-
-template <class Fmt, int R>
-__device__ __forceinline__ void shrink_fast(const KernelArgs& a, const DevItem& it,
-                                            const DevAdapter& ad, unsigned char* smem) {
-    constexpr int RT = kShrinkRowTile;
-    constexpr int VPR = R / 8;               // 16-byte vectors per row of A
-    constexpr int TPJ = kThreads / VPR;      // threads that share one octet of ranks
-    constexpr int KMAX = kChunkElems / R;    // rows of A in a full chunk
-    constexpr int M = KMAX / TPJ;            // vectors per thread (8)
-    static_assert(M * TPJ == KMAX, "chunk tiling");
-    static_assert(RT * KMAX * 2 <= kShrinkLdsBytes, "x tile fits");
-    static_assert(4 * RT * R * 4 <= kShrinkLdsBytes, "reduction fits");
-
-    const int t = threadIdx.x;
-    const int lane = t & 63;
-    const int w = t >> 6;
-    const int j0 = (t % VPR) * 8;
-    const int kr0 = t / VPR;
-    const int klen = it.len;
-    const uint16_t* A = (const uint16_t*)ad.A + (int64_t)it.lo * R;
-
-    // The whole chunk of A goes to registers first: every load in flight at once.
-    uint4 av[M];
+// Part q of the ordered sum of a row block's partial blocks at one position:
+// blocks q, q+P, q+2P, ... added in that order, eight loads in flight.
+__device__ __forceinline__ float part_sum(const float* src, int64_t pstride, int nsplit, int P,
+                                          int q, bool ok) {
+    float s = 0.f;
+    for (int c0 = q; c0 < nsplit; c0 += 8 * P) {
+        float u[8];
 #pragma unroll
-    for (int m = 0; m < M; ++m) {
-        const int kr = kr0 + m * TPJ;
-        av[m] = kr < klen ? *(const uint4*)(A + (int64_t)kr * R + j0) : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < 8; ++i) {
+            const int c = c0 + i * P;
+            u[i] = (ok && c < nsplit) ? src[(int64_t)c * pstride] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += u[i];
     }
+    return s;
+}
 
-    uint16_t* xs = (uint16_t*)smem;    // [RT][KMAX]
-    float* red = (float*)smem;         // [4][RT][R], reuses the x tile's bytes
-    const uint16_t* X = (const uint16_t*)a.x;
-    const int kv = klen / 8;
-    auto load_x_tile = [&](int i0, int nr) {
-        for (int idx = t; idx < nr * kv; idx += kThreads) {
-            const int r = idx / kv;
-            const int c = idx - r * kv;
-            const int64_t row = a.perm[it.p0 + i0 + r];
-            *(uint4*)(xs + r * KMAX + c * 8) = *(const uint4*)(X + row * a.ldx + it.lo + c * 8);
+// ---------------------------------------------------------------------------
+// Shrink
+// ---------------------------------------------------------------------------
+template <class Fmt, int TQ, int MS>
+__device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
+                                            unsigned char* smem) {
+    const int t = threadIdx.x;
+    const int w = t >> 6;
+    const int lr = t & 15;
+    const int lg = (t >> 4) & 3;
+    const int R = it.rank;
+    const int Rp = round_up_i(R, 16);
+    const int NT = Rp / 16;
+    const int sub = it.sub;                   // K staged per pass, multiple of 32
+    const int KP = shrink_kp(sub);            // words per A^T row, 4 (mod 8): conflict-free 16-byte reads
+    const int KX = shrink_kx(sub);            // halves per x row
+    const int nrows = it.nrows;
+    const int WN = shrink_wn(R);
+    const int WK = 4 / WN;
+    const int wn = w % WN;
+    const int wk = w / WN;
+    uint32_t* As = (uint32_t*)smem;                               // [Rp][KP] words
+    uint16_t* Xs = (uint16_t*)(smem + (size_t)Rp * KP * 4);       // [MS*16][KX]
+    gu16* A = item_factor(a, it, true) + (int64_t)it.lo * R;
+    const uint16_t* X = (const uint16_t*)a.x + it.lo;
+    const int rowv = lane_rows(a, it);
+    const u32x4 z4 = {0u, 0u, 0u, 0u};
+    const bool vec = (R & 7) == 0;
+    const int VPR = max_i(R / 8, 1);
+    const int npairs = vec ? (sub / 2) * VPR : 0;
+    const int kv = sub / 8;
+    const int nx = nrows * kv;
+    const int npass = (it.len + sub - 1) / sub;
+
+    // the padding ranks of A^T stay zero for every pass
+    for (int i = t; i < (Rp - R) * KP; i += kThreads) As[R * KP + i] = 0u;
+
+    u32x4 v0[4], v1[4], xv[4];
+    auto load_pass = [&](int pass) {
+        const int k0 = pass * sub;
+        const int plen = min_i(sub, it.len - k0);
+        const int lv = plen / 8;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int p = t + i * kThreads;
+            const int k2 = p / VPR;
+            const int k = 2 * k2;
+            const int jo = p - k2 * VPR;
+            const bool ok0 = p < npairs && k < plen;
+            const bool ok1 = p < npairs && k + 1 < plen;
+            // addresses stay inside A even where the load is masked off
+            gu16* src0 = A + (int64_t)(ok0 ? k0 + k : 0) * R + (ok0 ? jo * 8 : 0);
+            gu16* src1 = A + (int64_t)(ok1 ? k0 + k + 1 : 0) * R + (ok1 ? jo * 8 : 0);
+            v0[i] = ok0 ? *(gu32x4*)src0 : z4;
+            v1[i] = ok1 ? *(gu32x4*)src1 : z4;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int p = t + i * kThreads;
+            const int r = p < nx ? p / kv : 0;
+            const int c = p - r * kv;
+            const int row = row_of(rowv, r);
+            const bool ok = p < nx && c < lv;
+            xv[i] = ok ? *(const u32x4*)(X + (int64_t)row * a.ldx + k0 + (ok ? c * 8 : 0)) : z4;
+        }
+    };
+    auto store_x = [&]() {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int p = t + i * kThreads;
+            if (p < nx) {
+                const int r = p / kv;
+                *(u32x4*)(Xs + r * KX + (p - r * kv) * 8) = xv[i];
+            }
+        }
+    };
+    auto store_a = [&]() {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int p = t + i * kThreads;
+            if (p < npairs) {
+                const int k2 = p / VPR;
+                const int jo = p - k2 * VPR;
+                uint32_t* d = As + (jo * 8) * KP + k2;
+                d[0 * KP] = lo16(v0[i].x) | (v1[i].x << 16);
+                d[1 * KP] = hi16(v0[i].x) | (v1[i].x & 0xffff0000u);
+                d[2 * KP] = lo16(v0[i].y) | (v1[i].y << 16);
+                d[3 * KP] = hi16(v0[i].y) | (v1[i].y & 0xffff0000u);
+                d[4 * KP] = lo16(v0[i].z) | (v1[i].z << 16);
+                d[5 * KP] = hi16(v0[i].z) | (v1[i].z & 0xffff0000u);
+                d[6 * KP] = lo16(v0[i].w) | (v1[i].w << 16);
+                d[7 * KP] = hi16(v0[i].w) | (v1[i].w & 0xffff0000u);
+            }
+        }
+    };
+    // ranks that are not a multiple of 8: A^T element by element (correct, not tuned)
+    auto store_a_generic = [&](int pass) {
+        const int k0 = pass * sub;
+        const int plen = min_i(sub, it.len - k0);
+        for (int i = t; i < R * KP; i += kThreads) As[i] = 0u;
+        __syncthreads();
+        uint16_t* As16 = (uint16_t*)As;
+        gu16* src = A + (int64_t)k0 * R;
+        for (int e = t; e < plen * R; e += kThreads) {
+            const int k = e / R;
+            const int j = e - k * R;
+            As16[(j * KP) * 2 + k] = src[e];
         }
     };
 
-    // First x tile is requested while the A chunk is still in flight; A is
-    // widened to float32 once, after which its packed copy is dead.
-    load_x_tile(0, min(RT, it.nrows));
-    float af[M][8];
+    f32x4 acc[MS][TQ];
 #pragma unroll
-    for (int m = 0; m < M; ++m) unpack8<Fmt>(av[m], af[m]);
-    __syncthreads();
+    for (int m = 0; m < MS; ++m)
+#pragma unroll
+        for (int q = 0; q < TQ; ++q) acc[m][q] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int i0 = 0; i0 < it.nrows; i0 += RT) {
-        const int nr = min(RT, it.nrows - i0);
-        if (i0 > 0) {
-            __syncthreads();
-            load_x_tile(i0, nr);
-            __syncthreads();
+    load_pass(0);
+    for (int pass = 0; pass < npass; ++pass) {
+        if (pass > 0) __syncthreads();        // the previous pass's MFMA reads are done
+        if (vec) store_a();
+        else store_a_generic(pass);
+        store_x();
+        __syncthreads();
+        const int plen = min_i(sub, it.len - pass * sub);
+        if (pass + 1 < npass) load_pass(pass + 1);   // in flight during this pass's MFMA
+        const int ks = (plen + 31) / 32;
+        for (int s = wk; s < ks; s += WK) {
+            u32x4 af[TQ];
+#pragma unroll
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                af[q] = tile < NT ? *(const u32x4*)(As + (tile * 16 + lr) * KP + 16 * s + 4 * lg) : z4;
+            }
+#pragma unroll
+            for (int m = 0; m < MS; ++m) {
+                const int row = m * 16 + lr;
+                const u32x4 xf = row < nrows ? *(const u32x4*)(Xs + row * KX + 32 * s + 8 * lg) : z4;
+#pragma unroll
+                for (int q = 0; q < TQ; ++q) acc[m][q] = Fmt::mma32(af[q], xf, acc[m][q]);
+            }
         }
+    }
 
-        float acc[RT][8];
+    // lane holds v[row m*16+lr][ranks tile*16 + 4lg .. +3]
+    float* part = a.partials + it.part;
+    if (WK == 1) {
 #pragma unroll
-        for (int i = 0; i < RT; ++i)
+        for (int m = 0; m < MS; ++m) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[i][e] = 0.f;
-
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                const int row = m * 16 + lr;
+                if (tile < NT && row < nrows) {
+                    const int r0 = tile * 16 + 4 * lg;
+                    float* dst = part + row * R + r0;
+                    if ((R & 3) == 0 && r0 + 3 < R) {
+                        *(float4*)dst = make_float4(acc[m][q][0], acc[m][q][1], acc[m][q][2], acc[m][q][3]);
+                    } else {
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-            const int kr = kr0 + m * TPJ;
-            if (kr < klen) {
-#pragma unroll
-                for (int i = 0; i < RT; ++i) {
-                    if (i < nr) {
-                        const float xk = Fmt::to_f32(xs[i * KMAX + kr]);
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) acc[i][e] = fmaf(xk, af[m][e], acc[i][e]);
+                        for (int i = 0; i < 4; ++i)
+                            if (r0 + i < R) dst[i] = acc[m][q][i];
                     }
                 }
             }
         }
-
-        // lanes with the same rank octet within a wave: butterfly
+    } else {
+        __syncthreads();                      // staging is read no more
+        float* red = (float*)smem;            // [WK][MS*16][Rp]
 #pragma unroll
-        for (int mask = VPR; mask < 64; mask <<= 1)
+        for (int m = 0; m < MS; ++m) {
 #pragma unroll
-            for (int i = 0; i < RT; ++i)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[i][e] += __shfl_xor(acc[i][e], mask);
-
-        __syncthreads();   // x tile no longer read; its bytes become the reduction buffer
-        if (lane < VPR) {
-#pragma unroll
-            for (int i = 0; i < RT; ++i)
-                if (i < nr)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) red[(w * RT + i) * R + j0 + e] = acc[i][e];
-        }
-        __syncthreads();
-        for (int o = t; o < nr * R; o += kThreads) {
-            const int i = o / R;
-            const int j = o - i * R;
-            const float s = ((red[(0 * RT + i) * R + j] + red[(1 * RT + i) * R + j]) +
-                             red[(2 * RT + i) * R + j]) + red[(3 * RT + i) * R + j];
-            shrink_store(a, it, R, i0 + i, j, s);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Shrink, any rank in [1, 256] (correct, not tuned)
-// ---------------------------------------------------------------------------
-constexpr int kGenericRowTile = 2;
-constexpr int kGenericChunkElems = 8192;
-constexpr int kGenericLdsBytes = 2 * kGenericChunkElems + 2 * kGenericRowTile * 8192 + 4 * kThreads;
-
-template <class Fmt>
-__device__ void shrink_generic(const KernelArgs& a, const DevItem& it, const DevAdapter& ad,
-                               unsigned char* smem) {
-    const int R = ad.rank;
-    const int klen = it.len;
-    const int t = threadIdx.x;
-    // A chunk (klen*R <= kGenericChunkElems elements, a multiple of 8 and
-    // 16-byte aligned since k0 % 8 == 0), then the x rows, then the reduction.
-    uint16_t* as = (uint16_t*)smem;                                  // [kGenericChunkElems]
-    uint16_t* xs = as + kGenericChunkElems;                          // [2][klen <= 8192]
-    float* red = (float*)(smem + 2 * kGenericChunkElems + 2 * kGenericRowTile * 8192);   // [256]
-    const uint16_t* A = (const uint16_t*)ad.A + (int64_t)it.lo * R;
-    const int nvec = klen * R / 8;
-    __syncthreads();
-    for (int idx = t; idx < nvec; idx += kThreads) *(uint4*)(as + idx * 8) = *(const uint4*)(A + (int64_t)idx * 8);
-    const uint16_t* X = (const uint16_t*)a.x;
-    const int kv = klen / 8;
-    for (int i0 = 0; i0 < it.nrows; i0 += kGenericRowTile) {
-        const int nr = min(kGenericRowTile, it.nrows - i0);
-        __syncthreads();
-        for (int idx = t; idx < nr * kv; idx += kThreads) {
-            const int r = idx / kv;
-            const int c = idx - r * kv;
-            const int64_t row = a.perm[it.p0 + i0 + r];
-            *(uint4*)(xs + r * klen + c * 8) = *(const uint4*)(X + row * a.ldx + it.lo + c * 8);
-        }
-        __syncthreads();
-        const int NO = nr * R;
-        const int P = NO <= kThreads ? kThreads / NO : 1;   // threads per output
-        for (int ob = 0; ob < NO; ob += kThreads / P) {
-            const int o = ob + t % (kThreads / P);
-            const int part = t / (kThreads / P);
-            float acc = 0.f;
-            if (o < NO && part < P) {
-                const int i = o / R;
-                const int j = o - i * R;
-                for (int k = part; k < klen; k += P)
-                    acc = fmaf(Fmt::to_f32(xs[i * klen + k]), Fmt::to_f32(as[k * R + j]), acc);
-            }
-            __syncthreads();
-            red[t] = acc;
-            __syncthreads();
-            if (t < kThreads / P) {
-                const int oo = ob + t;
-                if (oo < NO) {
-                    float s = 0.f;
-                    for (int q = 0; q < P; ++q) s += red[q * (kThreads / P) + t];
-                    const int i = oo / R;
-                    shrink_store(a, it, R, i0 + i, oo - i * R, s);
-                }
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                if (tile < NT)
+                    *(float4*)(red + ((wk * MS + m) * 16 + lr) * Rp + tile * 16 + 4 * lg) =
+                        make_float4(acc[m][q][0], acc[m][q][1], acc[m][q][2], acc[m][q][3]);
             }
         }
+        __syncthreads();
+        for (int o = t; o < nrows * R; o += kThreads) {
+            const int row = o / R;
+            const int rank = o - row * R;
+            float s = red[row * Rp + rank];
+            for (int k = 1; k < WK; ++k) s += red[(k * MS * 16 + row) * Rp + rank];
+            part[o] = s;
+        }
     }
-}
-
-// ---------------------------------------------------------------------------
-// Split-K completion: the last workgroup of a group adds the partials in
-// chunk order into v and re-arms the group's counter for the next launch.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void shrink_finish(const KernelArgs& a, const DevItem& it, int R) {
-    const int nsplit = it.split & 0xffff;
-    if (nsplit == 1) return;
-    __shared__ int s_last;
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const int old = atomicAdd(&a.counters[it.group], 1);
-        s_last = (old == nsplit - 1);
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    const float* P = a.partials + a.part_off[it.group];
-    const int64_t per = (int64_t)it.nrows * R;
-    for (int o = threadIdx.x; o < per; o += kThreads) {
-        float s = 0.f;
-        for (int c = 0; c < nsplit; ++c) s += P[c * per + o];
-        const int i = o / R;
-        a.v[v_row(a, it.p0 + i) * a.ldv + (o - i * R)] = s;
-    }
-    if (threadIdx.x == 0)
-        __hip_atomic_store(&a.counters[it.group], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <class Fmt>
 __global__ void __launch_bounds__(kThreads) lora_shrink_kernel(KernelArgs a) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[kGenericLdsBytes > kShrinkLdsBytes ? kGenericLdsBytes : kShrinkLdsBytes];
-    const DevItem it = a.items[blockIdx.x];
-    const DevAdapter ad = a.table[it.adapter];
-    switch (ad.rank) {
-        case 8: shrink_fast<Fmt, 8>(a, it, ad, smem); break;
-        case 16: shrink_fast<Fmt, 16>(a, it, ad, smem); break;
-        case 32: shrink_fast<Fmt, 32>(a, it, ad, smem); break;
-        case 64: shrink_fast<Fmt, 64>(a, it, ad, smem); break;
-        case 128: shrink_fast<Fmt, 128>(a, it, ad, smem); break;
-        case 256: shrink_fast<Fmt, 256>(a, it, ad, smem); break;
-        default: shrink_generic<Fmt>(a, it, ad, smem); break;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kShrinkLds];
+    const Item it = load_item(a.items + blockIdx.x);
+    if (it.kind != kItemShrink) return;
+    const int tq = shrink_tq(it.rank);
+    const int ms = msub_body(it.nrows);
+    if (tq == 1) {
+        if (ms == 1) shrink_body<Fmt, 1, 1>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 1, 2>(a, it, smem);
+        else shrink_body<Fmt, 1, 4>(a, it, smem);
+    } else if (tq == 2) {
+        if (ms == 1) shrink_body<Fmt, 2, 1>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 2, 2>(a, it, smem);
+        else shrink_body<Fmt, 2, 4>(a, it, smem);
+    } else {
+        if (ms == 1) shrink_body<Fmt, 4, 1>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 4, 2>(a, it, smem);
+        else shrink_body<Fmt, 4, 4>(a, it, smem);
     }
-    shrink_finish(a, it, ad.rank);
 }
 
 // ---------------------------------------------------------------------------
-// Expand, rank R in {8,16,32,64,128,256}
+// Expand
 // ---------------------------------------------------------------------------
-template <class Fmt>
-__device__ __forceinline__ void y_update8(const KernelArgs& a, int64_t row, int col, float scale,
-                                          const float d[8]) {
-    uint16_t* Y = (uint16_t*)a.y + row * a.ldy + col;
-    const uint4 yv = *(const uint4*)Y;
-    float f[8];
-    unpack8<Fmt>(yv, f);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) f[c] = fmaf(scale, d[c], f[c]);
-    *(uint4*)Y = pack8<Fmt>(f);
-}
-
-template <class Fmt, int R>
-__device__ __forceinline__ void expand_fast(const KernelArgs& a, const DevItem& it,
-                                            const DevAdapter& ad, unsigned char* smem) {
-    constexpr int RT = kExpandRowTile;
-    constexpr int NMAX = kChunkElems / R;   // columns in a full tile
-    constexpr int CB = NMAX / 8;            // column blocks of 8
-    constexpr int JS = kThreads / CB;       // rank slices
-    static_assert(JS * 8 == R, "8 ranks per thread");
-    constexpr int WPC = CB >= 64 ? CB / 64 : 1;   // waves per column set
-    constexpr int NW = 4 / WPC;                   // partial sums per output after the wave step
-
+template <class Fmt, int Q, int MS>
+__device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
+                                            unsigned char* smem) {
     const int t = threadIdx.x;
-    const int lane = t & 63;
     const int w = t >> 6;
-    const int cb = t % CB;
-    const int js = t / CB;
-    const int nlen = it.len;
-    const bool col_ok = cb * 8 < nlen;
-    const int col = it.lo + cb * 8;
-    const uint16_t* B = (const uint16_t*)ad.B;
+    const int lr = t & 15;
+    const int lg = (t >> 4) & 3;
+    const int R = it.rank;
+    const int Rk = round_up_i(R, 16);
+    const int KS = Rk / 16;
+    const int half = Rk / 2;
+    const int RP = expand_rp(R);              // words per row: two ranks each, 2 (mod 4)
+    const int len = it.len;
+    const int ncol = round_up_i(len, 16);
+    const int NCT = ncol / 16;
+    const int nrows = it.nrows;
+    uint32_t* Bs = (uint32_t*)smem;           // [ncol][RP]  B^T, rank pairs
+    uint32_t* Vh = Bs + ncol * RP;            // [MS*16][RP]  high part of v
+    uint32_t* Vl = Vh + MS * 16 * RP;         // [MS*16][RP]  low part of v
+    float2* red = (float2*)(Vl + MS * 16 * RP);   // [kThreads]
+    gu16* B = item_factor(a, it, false);
+    const float scale = item_scale(a, it);
+    const int rowv = lane_rows(a, it);
+    const u32x4 z4 = {0u, 0u, 0u, 0u};
 
-    uint4 bv[8];
+    // --- requests: the B tile (<= 4 rank-pair loads per thread by the tiling) ...
+    const int cv = ncol / 8;                  // column octets
+    const int npairs = half * cv;
+    u32x4 b0[4], b1[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-        bv[e] = col_ok ? *(const uint4*)(B + (int64_t)(js * 8 + e) * a.h_out + col) : make_uint4(0, 0, 0, 0);
-    float bf[8][8];
+    for (int i = 0; i < 4; ++i) {
+        const int p = t + i * kThreads;
+        const int jp = p / cv;
+        const int co = p - jp * cv;
+        const int j = 2 * jp;
+        const bool ok0 = p < npairs && co * 8 < len && j < R;
+        const bool ok1 = p < npairs && co * 8 < len && j + 1 < R;
+        // addresses stay inside B even where the load is masked off
+        gu16* src0 = B + (int64_t)(ok0 ? j : 0) * a.h_out + it.lo + (ok0 ? co * 8 : 0);
+        gu16* src1 = B + (int64_t)(ok1 ? j + 1 : 0) * a.h_out + it.lo + (ok1 ? co * 8 : 0);
+        b0[i] = ok0 ? *(gu32x4*)src0 : z4;
+        b1[i] = ok1 ? *(gu32x4*)src1 : z4;
+    }
+    // ... this lane's y: rows m*16+lr, columns ct*16 + 4lg .. +3 of the wave's
+    // column tiles ct = w, w+4, ...
+    int yrow[MS];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) unpack8<Fmt>(bv[e], bf[e]);
-
-    float* vs = (float*)smem;                 // [RT][R]
-    float* red = vs + RT * kMaxRank;          // [NW][RT][NMAX]
-
-    for (int i0 = 0; i0 < it.nrows; i0 += RT) {
-        const int nr = min(RT, it.nrows - i0);
-        __syncthreads();
-        for (int o = t; o < nr * R; o += kThreads) {
-            const int i = o / R;
-            vs[o] = a.v[v_row(a, it.p0 + i0 + i) * a.ldv + (o - i * R)];
+    for (int m = 0; m < MS; ++m) yrow[m] = row_of(rowv, m * 16 + lr < nrows ? m * 16 + lr : 0);
+    u32x2 yv[Q][MS];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int ct = w + 4 * q;
+        const int c = ct * 16 + 4 * lg;
+#pragma unroll
+        for (int m = 0; m < MS; ++m) {
+            const bool ok = ct < NCT && m * 16 + lr < nrows && c + 4 <= len;
+            const uint16_t* src = (const uint16_t*)a.y + (int64_t)yrow[m] * a.ldy + it.lo + (ok ? c : 0);
+            yv[q][m] = ok ? *(const u32x2*)src : u32x2{0u, 0u};
         }
-        __syncthreads();
-        float acc[RT][8];
+    }
+    // ... and v: rank pairs of every row, the sum of the row block's partial
+    // blocks (or the caller's v).  With few slots, P threads share a slot,
+    // each adding every P-th block; the P sums are then added in order.
+    const int slots = nrows * half;
+    const int nslot = MS * 16 * half;
+    const int P = a.v ? 1 : partial_parts(nrows, R, it.nsplit);
+    const float* Pb = a.partials + it.part;
+    if (P > 1) {
+        const int slot = t % slots;
+        const int q = t / slots;
+        if (q < P) {
+            const int row = slot / half;
+            const int j = 2 * (slot - row * half);
+            const float* src = Pb + row * R;
+            const float s0 = part_sum(src + (j < R ? j : 0), it.pstride, it.nsplit, P, q, j < R);
+            const float s1 = part_sum(src + (j + 1 < R ? j + 1 : 0), it.pstride, it.nsplit, P, q, j + 1 < R);
+            red[t] = make_float2(s0, s1);
+        }
+    }
+
+    // --- B^T to LDS
 #pragma unroll
-        for (int i = 0; i < RT; ++i) {
-#pragma unroll
-            for (int c = 0; c < 8; ++c) acc[i][c] = 0.f;
-            if (i < nr) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float ve = vs[i * R + js * 8 + e];
-#pragma unroll
-                    for (int c = 0; c < 8; ++c) acc[i][c] = fmaf(ve, bf[e][c], acc[i][c]);
+    for (int i = 0; i < 4; ++i) {
+        const int p = t + i * kThreads;
+        if (p < npairs) {
+            const int jp = p / cv;
+            const int co = p - jp * cv;
+            uint32_t* d = Bs + (co * 8) * RP + jp;
+            d[0 * RP] = lo16(b0[i].x) | (b1[i].x << 16);
+            d[1 * RP] = hi16(b0[i].x) | (b1[i].x & 0xffff0000u);
+            d[2 * RP] = lo16(b0[i].y) | (b1[i].y << 16);
+            d[3 * RP] = hi16(b0[i].y) | (b1[i].y & 0xffff0000u);
+            d[4 * RP] = lo16(b0[i].z) | (b1[i].z << 16);
+            d[5 * RP] = hi16(b0[i].z) | (b1[i].z & 0xffff0000u);
+            d[6 * RP] = lo16(b0[i].w) | (b1[i].w << 16);
+            d[7 * RP] = hi16(b0[i].w) | (b1[i].w & 0xffff0000u);
+        }
+    }
+    if (P > 1) __syncthreads();               // the P-way sums are in red
+    // --- v to LDS as high / low 16-bit parts (rows past nrows: zero)
+    for (int o = t; o < nslot; o += kThreads) {
+        const int row = o / half;
+        const int jp = o - row * half;
+        const int j = 2 * jp;
+        float v0 = 0.f, v1 = 0.f;
+        if (row < nrows) {
+            if (a.v) {
+                const float* src = a.v + (int64_t)a.perm[it.p0 + row] * a.ldv;
+                if (j < R) v0 = src[j];
+                if (j + 1 < R) v1 = src[j + 1];
+            } else if (P > 1) {
+                for (int q = 0; q < P; ++q) {
+                    const float2 r2 = red[q * slots + o];
+                    v0 += r2.x;
+                    v1 += r2.y;
                 }
+            } else {
+                const float* src = Pb + row * R;
+                v0 += part_sum(src + (j < R ? j : 0), it.pstride, it.nsplit, 1, 0, j < R);
+                v1 += part_sum(src + (j + 1 < R ? j + 1 : 0), it.pstride, it.nsplit, 1, 0, j + 1 < R);
             }
         }
-        if constexpr (CB < 64) {
+        const uint32_t h0 = Fmt::from_f32(v0), h1 = Fmt::from_f32(v1);
+        const uint32_t l0 = Fmt::from_f32(v0 - Fmt::to_f32(h0));
+        const uint32_t l1 = Fmt::from_f32(v1 - Fmt::to_f32(h1));
+        Vh[row * RP + jp] = h0 | (h1 << 16);
+        Vl[row * RP + jp] = l0 | (l1 << 16);
+    }
+    __syncthreads();
+
+    // --- y^T = B^T v^T on MFMA, then y + s*d rounded once
+    f32x4 acc[Q][MS];
 #pragma unroll
-            for (int mask = CB; mask < 64; mask <<= 1)
+    for (int q = 0; q < Q; ++q)
 #pragma unroll
-                for (int i = 0; i < RT; ++i)
+        for (int m = 0; m < MS; ++m) acc[q][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < KS; ++s) {
+        u32x2 af[Q];
 #pragma unroll
-                    for (int c = 0; c < 8; ++c) acc[i][c] += __shfl_xor(acc[i][c], mask);
+        for (int q = 0; q < Q; ++q) {
+            const int ct = w + 4 * q;
+            af[q] = ct < NCT ? *(const u32x2*)(Bs + (ct * 16 + lr) * RP + 8 * s + 2 * lg) : u32x2{0u, 0u};
         }
-        if constexpr (NW == 1) {
-            if (col_ok) {
 #pragma unroll
-                for (int i = 0; i < RT; ++i)
-                    if (i < nr) y_update8<Fmt>(a, a.perm[it.p0 + i0 + i], col, ad.scale, acc[i]);
+        for (int m = 0; m < MS; ++m) {
+            const u32x2 bh = *(const u32x2*)(Vh + (m * 16 + lr) * RP + 8 * s + 2 * lg);
+            const u32x2 bl = *(const u32x2*)(Vl + (m * 16 + lr) * RP + 8 * s + 2 * lg);
+#pragma unroll
+            for (int q = 0; q < Q; ++q) {
+                acc[q][m] = Fmt::mma16(af[q], bh, acc[q][m]);
+                acc[q][m] = Fmt::mma16(af[q], bl, acc[q][m]);
             }
-        } else {
-            const int q = CB >= 64 ? w / WPC : w;
-            const bool writer = CB >= 64 ? true : lane < CB;
-            const int cbw = CB >= 64 ? (w % WPC) * 64 + lane : lane;
-            if (writer) {
+        }
+    }
 #pragma unroll
-                for (int i = 0; i < RT; ++i)
-                    if (i < nr)
+    for (int q = 0; q < Q; ++q) {
+        const int ct = w + 4 * q;
+        const int c = ct * 16 + 4 * lg;
 #pragma unroll
-                        for (int c = 0; c < 8; ++c) red[(q * RT + i) * NMAX + cbw * 8 + c] = acc[i][c];
-            }
-            __syncthreads();
-            for (int o = t; o < nr * CB; o += kThreads) {
-                const int i = o / CB;
-                const int b = o - i * CB;
-                if (b * 8 < nlen) {
-                    float d[8];
-#pragma unroll
-                    for (int c = 0; c < 8; ++c) {
-                        float s = red[(0 * RT + i) * NMAX + b * 8 + c];
-#pragma unroll
-                        for (int qq = 1; qq < NW; ++qq) s += red[(qq * RT + i) * NMAX + b * 8 + c];
-                        d[c] = s;
-                    }
-                    y_update8<Fmt>(a, a.perm[it.p0 + i0 + i], it.lo + b * 8, ad.scale, d);
-                }
+        for (int m = 0; m < MS; ++m) {
+            if (ct < NCT && m * 16 + lr < nrows && c + 4 <= len) {
+                const u32x2 yo = yv[q][m];
+                const float f0 = fmaf(scale, acc[q][m][0], Fmt::to_f32(lo16(yo.x)));
+                const float f1 = fmaf(scale, acc[q][m][1], Fmt::to_f32(hi16(yo.x)));
+                const float f2 = fmaf(scale, acc[q][m][2], Fmt::to_f32(lo16(yo.y)));
+                const float f3 = fmaf(scale, acc[q][m][3], Fmt::to_f32(hi16(yo.y)));
+                *(u32x2*)((uint16_t*)a.y + (int64_t)yrow[m] * a.ldy + it.lo + c) =
+                    u32x2{Fmt::from_f32(f0) | (Fmt::from_f32(f1) << 16),
+                          Fmt::from_f32(f2) | (Fmt::from_f32(f3) << 16)};
             }
         }
     }
 }
-
-// ---------------------------------------------------------------------------
-// Expand, any rank in [1, 256] (correct, not tuned)
-// ---------------------------------------------------------------------------
-template <class Fmt>
-__device__ void expand_generic(const KernelArgs& a, const DevItem& it, const DevAdapter& ad,
-                               unsigned char* smem) {
-    constexpr int RT = kExpandRowTile;
-    const int R = ad.rank;
-    const int t = threadIdx.x;
-    float* vs = (float*)smem;   // [RT][R]
-    const uint16_t* B = (const uint16_t*)ad.B;
-    for (int i0 = 0; i0 < it.nrows; i0 += RT) {
-        const int nr = min(RT, it.nrows - i0);
-        __syncthreads();
-        for (int o = t; o < nr * R; o += kThreads) {
-            const int i = o / R;
-            vs[o] = a.v[v_row(a, it.p0 + i0 + i) * a.ldv + (o - i * R)];
-        }
-        __syncthreads();
-        for (int c = t; c < it.len; c += kThreads) {
-            const int col = it.lo + c;
-            float acc[RT];
-#pragma unroll
-            for (int i = 0; i < RT; ++i) acc[i] = 0.f;
-            for (int j = 0; j < R; ++j) {
-                const float b = Fmt::to_f32(B[(int64_t)j * a.h_out + col]);
-#pragma unroll
-                for (int i = 0; i < RT; ++i)
-                    if (i < nr) acc[i] = fmaf(vs[i * R + j], b, acc[i]);
-            }
-#pragma unroll
-            for (int i = 0; i < RT; ++i) {
-                if (i < nr) {
-                    uint16_t* Y = (uint16_t*)a.y + (int64_t)a.perm[it.p0 + i0 + i] * a.ldy + col;
-                    *Y = (uint16_t)Fmt::from_f32(fmaf(ad.scale, acc[i], Fmt::to_f32(*Y)));
-                }
-            }
-        }
-    }
-}
-
-constexpr int kExpandLdsBytes = (kExpandRowTile * kMaxRank + 4 * kExpandRowTile * 512) * 4;
 
 template <class Fmt>
 __global__ void __launch_bounds__(kThreads) lora_expand_kernel(KernelArgs a) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLdsBytes];
-    const DevItem it = a.items[blockIdx.x];
-    const DevAdapter ad = a.table[it.adapter];
-    switch (ad.rank) {
-        case 8: expand_fast<Fmt, 8>(a, it, ad, smem); break;
-        case 16: expand_fast<Fmt, 16>(a, it, ad, smem); break;
-        case 32: expand_fast<Fmt, 32>(a, it, ad, smem); break;
-        case 64: expand_fast<Fmt, 64>(a, it, ad, smem); break;
-        case 128: expand_fast<Fmt, 128>(a, it, ad, smem); break;
-        case 256: expand_fast<Fmt, 256>(a, it, ad, smem); break;
-        default: expand_generic<Fmt>(a, it, ad, smem); break;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLds];
+    const Item it = load_item(a.items + blockIdx.x);
+    if (it.kind != kItemExpand) return;
+    const int q = (round_up_i(it.len, 16) / 16 + 3) / 4;   // column tiles per wave
+    const int ms = msub_body(it.nrows);
+    if (ms == 1) {
+        if (q <= 1) expand_body<Fmt, 1, 1>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 1>(a, it, smem);
+        else if (q <= 4) expand_body<Fmt, 4, 1>(a, it, smem);
+        else expand_body<Fmt, 8, 1>(a, it, smem);
+    } else if (ms == 2) {
+        if (q <= 1) expand_body<Fmt, 1, 2>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 2>(a, it, smem);
+        else if (q <= 4) expand_body<Fmt, 4, 2>(a, it, smem);
+        else expand_body<Fmt, 8, 2>(a, it, smem);
+    } else {
+        if (q <= 1) expand_body<Fmt, 1, 4>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 4>(a, it, smem);
+        else expand_body<Fmt, 4, 4>(a, it, smem);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Reduce: v(rows, 0:r) = sum of the row block's partial blocks, in order (the
+// standalone shrink's output).
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kThreads) lora_reduce_kernel(KernelArgs a) {
+    const Item it = load_item(a.items + blockIdx.x);
+    if (it.kind != kItemReduce) return;
+    const int R = it.rank;
+    const int n = it.nrows * R;
+    const float* Pb = a.partials + it.part;
+    const int P = partial_parts(it.nrows, R, it.nsplit);   // the expand's order
+    for (int o = threadIdx.x; o < n; o += kThreads) {
+        float s = 0.f;
+        for (int q = 0; q < P; ++q) s += part_sum(Pb + o, it.pstride, it.nsplit, P, q, true);
+        const int i = o / R;
+        a.v[(int64_t)a.perm[it.p0 + i] * a.ldv + (o - i * R)] = s;
     }
 }
 
@@ -493,6 +617,12 @@ hipError_t launch_expand(const KernelArgs& a, int dtype, hipStream_t s) {
         hipLaunchKernelGGL(lora_expand_kernel<FmtF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
     else
         hipLaunchKernelGGL(lora_expand_kernel<FmtBF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce(const KernelArgs& a, hipStream_t s) {
+    if (a.n_items <= 0) return hipSuccess;
+    hipLaunchKernelGGL(lora_reduce_kernel, dim3(a.n_items), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

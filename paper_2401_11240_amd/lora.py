@@ -98,10 +98,10 @@ def load():
         "lora_expand": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_apply_fused": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
-        "lora_plan_apply": [vp, vp, i64, vp, i64, vp],
+        "lora_plan_apply": [vp, vp, vp, i64, vp, i64, vp],
         "lora_plan_destroy": [vp],
-        "lora_plan_shrink": [vp, vp, i64, vp],
-        "lora_plan_expand": [vp, vp, i64, vp],
+        "lora_plan_shrink": [vp, vp, vp, i64, vp],
+        "lora_plan_expand": [vp, vp, vp, i64, vp],
         "lora_group_rows": [C.POINTER(_Batch), i32, i32p, i32p, i32p, i32p],
         "lora_last_error": [],
         "lora_abi_version": [],
@@ -193,16 +193,17 @@ def lora_plan_create(table: int, batch: Batch, stream=None) -> int:
     return out.value
 
 
-def lora_plan_apply(plan: int, x, ldx: int, y, ldy: int, stream=None) -> None:
-    _check(load().lora_plan_apply(plan, _addr(x), ldx, _addr(y), ldy, _stream(stream)))
+def lora_plan_apply(plan: int, table, x, ldx: int, y, ldy: int, stream=None) -> None:
+    """``table`` None = the table the plan was made with."""
+    _check(load().lora_plan_apply(plan, table or None, _addr(x), ldx, _addr(y), ldy, _stream(stream)))
 
 
-def lora_plan_shrink(plan: int, x, ldx: int, stream=None) -> None:
-    _check(load().lora_plan_shrink(plan, _addr(x), ldx, _stream(stream)))
+def lora_plan_shrink(plan: int, table, x, ldx: int, stream=None) -> None:
+    _check(load().lora_plan_shrink(plan, table or None, _addr(x), ldx, _stream(stream)))
 
 
-def lora_plan_expand(plan: int, y, ldy: int, stream=None) -> None:
-    _check(load().lora_plan_expand(plan, _addr(y), ldy, _stream(stream)))
+def lora_plan_expand(plan: int, table, y, ldy: int, stream=None) -> None:
+    _check(load().lora_plan_expand(plan, table or None, _addr(y), ldy, _stream(stream)))
 
 
 def lora_plan_destroy(plan: int) -> None:

@@ -257,12 +257,55 @@ def test_plan_reuse_and_determinism():
     try:
         for rep in range(3):   # the split-K counters must re-arm between launches
             y = p.y.clone()
-            L.lora_plan_apply(plan, x, x.shape[1], y, y.shape[1], stream())
+            L.lora_plan_apply(plan, None, x, x.shape[1], y, y.shape[1], stream())
             torch.cuda.synchronize()
             assert np.array_equal(D.from_device_bits(y), ref), rep
     finally:
         L.lora_plan_destroy(plan)
     dw.release()
+
+
+def test_plan_runs_on_other_compatible_tables():
+    """A plan depends on the batch and ranks only: applied to another table
+    with the same ranks (another layer's factors) it gives that table's
+    result; a table with another rank is refused before anything runs."""
+    c = RANDOM_CASES[1]
+    w1 = random_workload(c)
+    w2 = W.build_workload(name="other_layer", seed=77, dtype=w1.dtype, n_adapters=w1.n_adapters,
+                          fixed_ranks=w1.ranks, seg_adapter=w1.seg_adapter,
+                          seg_lens=np.diff(w1.seg_offset), projections=(("proj", c[2], c[3], "x"),))
+    d1 = D.upload(w1, DEV)
+    d2 = D.upload(w2, DEV)
+    ref2 = run_fused(d2, "proj")
+    p1, p2 = d1.projection("proj"), d2.projection("proj")
+    plan = L.lora_plan_create(p1.table, d1.batch, stream())
+    try:
+        x2 = d2.xs["x"]
+        y2 = p2.y.clone()
+        L.lora_plan_apply(plan, p2.table, x2, x2.shape[1], y2, y2.shape[1], stream())
+        torch.cuda.synchronize()
+        assert np.array_equal(D.from_device_bits(y2), ref2)
+        # shrink then expand as two launches: the same bits
+        y3 = p2.y.clone()
+        L.lora_plan_shrink(plan, p2.table, x2, x2.shape[1], stream())
+        L.lora_plan_expand(plan, p2.table, y3, y3.shape[1], stream())
+        torch.cuda.synchronize()
+        assert np.array_equal(D.from_device_bits(y3), ref2)
+        ranks3 = w1.ranks.copy()
+        used = int(w1.seg_adapter[w1.seg_adapter >= 0][0])
+        ranks3[used] = 8 if ranks3[used] != 8 else 16
+        bad = L.lora_register_adapters(0, c[2], c[3], w1.dtype, p1.A_ptrs, p1.B_ptrs, ranks3,
+                                       w1.scales, stream())
+        try:
+            with pytest.raises(L.LoraError) as e:
+                L.lora_plan_apply(plan, bad, x2, x2.shape[1], y2, y2.shape[1], stream())
+            assert e.value.code == L.LORA_E_RANK
+        finally:
+            L.lora_release_adapters(bad)
+    finally:
+        L.lora_plan_destroy(plan)
+    d1.release()
+    d2.release()
 
 
 def test_permutation_invariance_bit_exact():
