@@ -128,7 +128,8 @@ __device__ __forceinline__ float item_scale(const KernelArgs& a, const Item& it)
 // v with lane Q replaced by the wave-uniform value s (one VALU lane write).
 template <int Q>
 __device__ __forceinline__ int write_lane(int v, int s) {
-    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(s), "n"(Q));
+    const int su = __builtin_amdgcn_readfirstlane(s);   // the operand must be a scalar register
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(su), "n"(Q));
     return v;
 }
 template <int Q>
