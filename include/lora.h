@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define LORA_ABI_VERSION 1
+#define LORA_ABI_VERSION 2
 
 typedef enum { LORA_F16 = 0, LORA_BF16 = 1 } lora_dtype_t;
 
@@ -71,7 +71,8 @@ enum {
     LORA_E_NOMEM = -6,      /* host or device allocation failed                  */
     LORA_E_HIP = -7,        /* a HIP runtime call or kernel launch failed        */
     LORA_E_WORKSPACE = -8,  /* workspace smaller than lora_workspace_bytes()     */
-    LORA_E_OVERLAP = -9     /* x and y overlap                                   */
+    LORA_E_OVERLAP = -9,    /* x and y overlap                                   */
+    LORA_E_SYNC = -10       /* a step launch gave up waiting (lora_plan_status)  */
 };
 
 /* A step's batch, in HOST memory; read during the call only. */
@@ -141,9 +142,22 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
  * uploads it, with its own workspace, to device memory owned by the plan
  * (allocates; not for the hot loop).
  *
- * lora_plan_apply runs the whole delta (lora_apply_fused without the upload:
- * it enqueues kernels only) with the adapters of table t, or of the table the
- * plan was made with when t is NULL.  Any table with the same h_in, h_out and
+ * lora_plan_apply runs the whole delta (lora_apply_fused without the upload)
+ * with the adapters of table t, or of the table the plan was made with when t
+ * is NULL, as ONE kernel launch: its grid holds the shrink work items, then
+ * the expand work items.  The float32 partial blocks of this launch live in
+ * plan memory armed with a sentinel bit pattern (all ones, a NaN that no
+ * 16-bit input can produce).  A shrink workgroup writes its block with
+ * device-coherent stores; an expand workgroup requests its B tile and its y
+ * values, then loads the partial values it needs, again while any still holds
+ * the sentinel; the last expand item of a row block arms its blocks again.  A
+ * workgroup waits only for workgroups earlier in the grid, which never wait,
+ * and the wait is bounded: past lora_plan_set_spin_limit polling rounds per
+ * thread (default 2^18, about a quarter of a second) it gives up, raises the
+ * plan's status flag and finishes with invalid results, which
+ * lora_plan_status reports.  The partial blocks are added in a fixed order,
+ * so the result is the same bits as lora_plan_shrink followed by
+ * lora_plan_expand, whatever the timing.  Any table with the same h_in, h_out and
  * dtype whose adapters referenced by the batch have the same ranks may be
  * used (e.g. the same adapters' factors in another layer); the weight
  * pointers and scales travel in the launch arguments.  A mismatch returns
@@ -163,6 +177,22 @@ int lora_plan_apply(lora_plan_t p, lora_table_t t, const void* x, int64_t ldx, v
 int lora_plan_shrink(lora_plan_t p, lora_table_t t, const void* x, int64_t ldx, void* stream);
 int lora_plan_expand(lora_plan_t p, lora_table_t t, void* y, int64_t ldy, void* stream);
 int lora_plan_destroy(lora_plan_t p);
+
+/*
+ * Status of the plan's step launches so far: waits for `stream`, then returns
+ * LORA_OK, or LORA_E_SYNC when a lora_plan_apply launch gave up waiting (its
+ * y is invalid); the flag, the row block counters and the sentinel are then
+ * reset, so the plan is usable again.  Host-synchronising: call it off the
+ * hot loop.
+ */
+int lora_plan_status(lora_plan_t p, void* stream);
+
+/*
+ * Polling rounds per thread after which a step launch's wait gives up (>= 0;
+ * applies to later lora_plan_apply calls).  Returns LORA_E_ARG for a NULL
+ * plan or a negative count.
+ */
+int lora_plan_set_spin_limit(lora_plan_t p, int32_t polls);
 
 /*
  * The integer part of the plan, on the host only (no GPU needed): rows that

@@ -24,6 +24,7 @@ namespace lora {
 hipError_t launch_shrink(const KernelArgs& a, int dtype, hipStream_t s);
 hipError_t launch_expand(const KernelArgs& a, int dtype, hipStream_t s);
 hipError_t launch_reduce(const KernelArgs& a, hipStream_t s);
+hipError_t launch_step(const KernelArgs& a, int dtype, hipStream_t s);
 }  // namespace lora
 
 using namespace lora;
@@ -51,6 +52,11 @@ inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 
 // Workgroups the planner aims for when it sizes the K ranges of prompt-sized
 // row blocks (two per CU on a 256-CU device).
 constexpr int kTargetItems = 512;
+
+// Polling rounds a step launch's thread may spend waiting before it gives up
+// (each round is a device-coherent load, about a microsecond under load), in
+// all: a quarter of a second, against waits of microseconds.
+constexpr int kSpinLimit = 1 << 18;
 
 struct DeviceGuard {
     int prev = -1;
@@ -87,11 +93,13 @@ struct HostPlan {
     int n_active = 0;
     int n_groups = 0;
     int r_max = 0;
+    int n_rb = 0;                       // row blocks
     std::vector<int32_t> perm, group_off, group_adapter, group_rank;
     std::vector<DevItem> shrink, expand, reduce;
     int64_t n_partials = 0;
     size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_perm = 0;
-    size_t plan_bytes = 0, off_partials = 0, total_bytes = 0;
+    size_t plan_bytes = 0, off_partials = 0, off_sync = 0, sync_bytes = 0, total_bytes = 0;
+    size_t off_step_partials = 0, step_partials_bytes = 0, plan_total_bytes = 0;
     std::vector<unsigned char> blob;
 };
 
@@ -162,6 +170,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.expand.clear();
     p.reduce.clear();
     p.n_partials = 0;
+    p.n_rb = 0;
 
     // Prompt-sized row blocks (more than 16 rows) stream their K range in
     // several passes; how many K ranges they are cut into follows from how
@@ -195,6 +204,8 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
             const int nlen = expand_nlen(r, nb);
             const int ntiles = (t->h_out + nlen - 1) / nlen;
             DevItem base{};
+            base.rb = p.n_rb++;
+            base.nexp = ntiles;
             base.group = g;
             base.adapter = p.group_adapter[g];
             base.rank = r;
@@ -234,10 +245,14 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
         }
     }
 
-    // device layout: [shrink items][expand items][reduce items][perm] | [partials]
+    // device layout: [shrink items][expand items][reduce items][perm] |
+    // [partials][row block counters, status] (a workspace ends here) |
+    // [step partials] (plans only: the step launch's partial blocks, armed
+    // with the sentinel between launches).  The expand items follow the shrink
+    // items directly: the step launch runs both lists as one grid.
     size_t off = 0;
     p.off_shrink = off;
-    off = align_up(off + p.shrink.size() * sizeof(DevItem));
+    off += p.shrink.size() * sizeof(DevItem);
     p.off_expand = off;
     off = align_up(off + p.expand.size() * sizeof(DevItem));
     p.off_reduce = off;
@@ -247,7 +262,13 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.plan_bytes = off;
     p.off_partials = off;
     off = align_up(off + (size_t)p.n_partials * sizeof(float));
+    p.off_sync = off;
+    p.sync_bytes = align_up(((size_t)p.n_rb + 1) * sizeof(uint32_t));
+    off += p.sync_bytes;
     p.total_bytes = std::max<size_t>(off, kAlign);
+    p.off_step_partials = off;
+    p.step_partials_bytes = align_up((size_t)p.n_partials * sizeof(float));
+    p.plan_total_bytes = std::max<size_t>(off + p.step_partials_bytes, kAlign);
 
     p.blob.assign(p.plan_bytes, 0);
     auto put = [&](size_t at, const void* src, size_t n) {
@@ -320,19 +341,23 @@ int stage_upload(int device, const void* src, size_t bytes, void* dst, hipStream
 }
 
 // Launch arguments of one plan on one table: the plan's buffers in workspace
-// w, and the group pointer table of the shrink (A) or expand (B) factors.
-KernelArgs make_args(const lora_table_s* t, const HostPlan& p, unsigned char* w, bool shrink_side) {
+// w and the factor pointers and scales of its groups.
+KernelArgs make_args(const lora_table_s* t, const HostPlan& p, unsigned char* w, int spin_limit) {
     KernelArgs a{};
     a.perm = (const int32_t*)(w + p.off_perm);
     a.table = t->dev;
     a.partials = (float*)(w + p.off_partials);
+    a.sync = (uint32_t*)(w + p.off_sync);
+    a.status = (int32_t*)(a.sync + p.n_rb);
+    a.spin_limit = spin_limit;
     a.h_in = t->h_in;
     a.h_out = t->h_out;
     a.n_groups = p.n_groups;
     const int ng = std::min(p.n_groups, kKargGroups);
     for (int g = 0; g < ng; ++g) {
         const DevAdapter& ad = t->host[p.group_adapter[g]];
-        a.gptr[g] = shrink_side ? ad.A : ad.B;
+        a.gfac[2 * g] = ad.A;
+        a.gfac[2 * g + 1] = ad.B;
         a.gscale[g] = ad.scale;
     }
     return a;
@@ -390,11 +415,11 @@ int check_v(const HostPlan& p, const void* v, int64_t ldv) {
 }
 
 // Enqueue the shrink (x != NULL) and/or the expand (y != NULL) of plan p on
-// table t with its workspace at w.
+// table t with its workspace at w, as two launches.
 int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x, int64_t ldx,
             void* y, int64_t ldy, hipStream_t s) {
     if (x) {
-        KernelArgs a = make_args(t, p, w, true);
+        KernelArgs a = make_args(t, p, w, kSpinLimit);
         a.items = (const DevItem*)(w + p.off_shrink);
         a.n_items = (int32_t)p.shrink.size();
         a.x = x;
@@ -402,7 +427,7 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
         LORA_HIP_TRY(launch_shrink(a, t->dtype, s));
     }
     if (y) {
-        KernelArgs a = make_args(t, p, w, false);
+        KernelArgs a = make_args(t, p, w, kSpinLimit);
         a.items = (const DevItem*)(w + p.off_expand);
         a.n_items = (int32_t)p.expand.size();
         a.y = y;
@@ -410,6 +435,33 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
         LORA_HIP_TRY(launch_expand(a, t->dtype, s));
     }
     return LORA_OK;
+}
+
+// Enqueue the whole step of plan p as one launch (shrink and expand items in
+// one grid).  The row block counters at w + off_sync must be zero and the
+// step partial blocks armed.
+int enqueue_step(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x,
+                 int64_t ldx, void* y, int64_t ldy, int spin_limit, hipStream_t s) {
+    KernelArgs a = make_args(t, p, w, spin_limit);
+    a.partials = (float*)(w + p.off_step_partials);
+    a.items = (const DevItem*)(w + p.off_shrink);
+    a.n_items = (int32_t)(p.shrink.size() + p.expand.size());
+    a.x = x;
+    a.ldx = ldx;
+    a.y = y;
+    a.ldy = ldy;
+    LORA_HIP_TRY(launch_step(a, t->dtype, s));
+    return LORA_OK;
+}
+
+// Counters and status to zero, step partial blocks to the sentinel (all-ones
+// bytes).  Plan creation and the status reset only, never inside a launch
+// sequence a caller may capture.
+hipError_t arm_step(const HostPlan& p, unsigned char* w, hipStream_t s) {
+    hipError_t e = hipMemsetAsync(w + p.off_sync, 0, p.sync_bytes, s);
+    if (e == hipSuccess && p.step_partials_bytes)
+        e = hipMemsetAsync(w + p.off_step_partials, 0xff, p.step_partials_bytes, s);
+    return e;
 }
 
 }  // namespace
@@ -420,6 +472,7 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
 struct lora_plan_s {
     const lora_table_s* table = nullptr;
     int n_rows = 0;
+    int spin_limit = kSpinLimit;
     HostPlan plan;
     unsigned char* dmem = nullptr;
 };
@@ -537,7 +590,7 @@ int lora_shrink(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ld
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
     if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s)) return rc;
-    KernelArgs a = make_args(t, p, w, true);
+    KernelArgs a = make_args(t, p, w, kSpinLimit);
     a.items = (const DevItem*)(w + p.off_reduce);
     a.n_items = (int32_t)p.reduce.size();
     a.v = v;
@@ -559,7 +612,7 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
     hipStream_t s = (hipStream_t)stream;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
-    KernelArgs a = make_args(t, p, w, false);
+    KernelArgs a = make_args(t, p, w, kSpinLimit);
     a.items = (const DevItem*)(w + p.off_expand);
     a.n_items = (int32_t)p.expand.size();
     a.v = const_cast<float*>(v);
@@ -600,13 +653,14 @@ int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, vo
     }
     pl->n_rows = b->n_rows;
     DeviceGuard dg(t->device);
-    hipError_t e = hipMalloc((void**)&pl->dmem, pl->plan.total_bytes);
+    hipError_t e = hipMalloc((void**)&pl->dmem, pl->plan.plan_total_bytes);
     if (e != hipSuccess) {
         delete pl;
         return fail(LORA_E_NOMEM, std::string("hipMalloc of the plan: ") + hipGetErrorString(e));
     }
     hipStream_t s = (hipStream_t)stream;
     e = hipMemcpyAsync(pl->dmem, pl->plan.blob.data(), pl->plan.plan_bytes, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = arm_step(pl->plan, pl->dmem, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
         (void)hipFree(pl->dmem);
@@ -630,6 +684,8 @@ static int plan_run(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, 
     if (x && y)
         if (int rc = check_overlap(x, ldx, tt->h_in, y, ldy, tt->h_out, pl->n_rows)) return rc;
     DeviceGuard dg(tt->device);
+    if (x && y)
+        return enqueue_step(tt, pl->plan, pl->dmem, x, ldx, y, ldy, pl->spin_limit, (hipStream_t)stream);
     return enqueue(tt, pl->plan, pl->dmem, x, ldx, y, ldy, (hipStream_t)stream);
 }
 
@@ -647,6 +703,28 @@ int lora_plan_shrink(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx,
 int lora_plan_expand(lora_plan_t pl, lora_table_t t, void* y, int64_t ldy, void* stream) {
     if (!y) return fail(LORA_E_ARG, "y is NULL");
     return plan_run(pl, t, nullptr, 0, y, ldy, stream);
+}
+
+int lora_plan_status(lora_plan_t pl, void* stream) {
+    if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
+    DeviceGuard dg(pl->table->device);
+    hipStream_t s = (hipStream_t)stream;
+    const HostPlan& p = pl->plan;
+    int32_t flag = 0;
+    LORA_HIP_TRY(hipMemcpyAsync(&flag, pl->dmem + p.off_sync + p.n_rb * sizeof(uint32_t), sizeof(flag),
+                                hipMemcpyDeviceToHost, s));
+    LORA_HIP_TRY(hipStreamSynchronize(s));
+    if (flag == 0) return LORA_OK;
+    LORA_HIP_TRY(arm_step(p, pl->dmem, s));
+    LORA_HIP_TRY(hipStreamSynchronize(s));
+    return fail(LORA_E_SYNC, "a step launch gave up waiting for its shrink items; its results are invalid");
+}
+
+int lora_plan_set_spin_limit(lora_plan_t pl, int32_t polls) {
+    if (!pl) return fail(LORA_E_ARG, "plan is NULL");
+    if (polls < 0) return fail(LORA_E_ARG, "negative spin limit");
+    pl->spin_limit = polls;
+    return LORA_OK;
 }
 
 int lora_plan_destroy(lora_plan_t pl) {

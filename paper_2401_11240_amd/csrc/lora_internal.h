@@ -11,10 +11,15 @@
 // Section 5), and items of every rank run side by side in one grid.
 //
 // The shrink writes one float32 partial block per (row block, K range); the
-// expand adds a row block's partial blocks in a fixed order while it stages v.
-// No workgroup ever waits for another: the boundary between the shrink and
-// the expand launches is the only synchronisation, so results never depend on
-// timing.
+// expand adds a row block's partial blocks in a fixed order while it stages v,
+// so results never depend on timing.  The two run either as two launches (the
+// launch boundary orders them) or as one step launch whose grid holds every
+// shrink item before every expand item: a shrink workgroup writes its block
+// with device-coherent stores into a buffer armed with a sentinel pattern; an
+// expand workgroup requests its B tile and its y values, then loads the
+// partial values, again while any still holds the sentinel.  It only ever
+// waits for workgroups earlier in the grid, which never wait themselves, and
+// the wait is bounded (it gives up and raises a status flag).
 //
 // A plan depends on the batch, the ranks and the shapes only.  The weight
 // pointers and scales of the groups it references travel in the kernel
@@ -40,9 +45,10 @@ constexpr int kThreads = 256;            // workgroup size: 4 wave64
 constexpr int kMaxRank = 256;
 constexpr int kMSub = 4;                 // 16-row MFMA subtiles per item at most
 constexpr int kInlineRows = 16;          // items this small carry their rows inline
-constexpr int kKargGroups = 192;         // group pointers passed in the kernel arguments
+constexpr int kKargGroups = 128;         // groups whose pointers travel in the kernel arguments
 constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink kernel
 constexpr int kExpandLds = 68 * 1024;    // LDS bytes of the expand kernel
+constexpr int kStepLds = kExpandLds > kShrinkLds ? kExpandLds : kShrinkLds;
 
 // Item kinds.
 enum : int32_t {
@@ -76,7 +82,9 @@ struct DevItem {
     int32_t nsplit;      // expand / reduce: partial blocks to add
     int32_t p0;          // position of the first row in the grouped row order (perm)
     int32_t pstride;     // floats between consecutive partial blocks of the row block
-    int32_t pad[3];
+    int32_t rb;          // row block index (its departure counter in the step launch)
+    int32_t nexp;        // expand items of the row block
+    int32_t pad;
     int32_t rows[kInlineRows];   // the item's rows when nrows <= kInlineRows
 };
 static_assert(sizeof(DevItem) == 128, "DevItem layout");
@@ -96,9 +104,14 @@ struct KernelArgs {
     int32_t h_out;
     int32_t n_items;
     int32_t n_groups;
-    const void* gptr[kKargGroups];   // per group: A_g (shrink launch) or B_g (expand launch)
-    float gscale[kKargGroups];       // per group: s_g
+    uint32_t* sync;             // step launch: per row block, expand items done; zero between launches
+    int32_t* status;            // step launch: set to 1 when a wait gave up
+    int32_t spin_limit;         // step launch: polling rounds before a wait gives up
+    int32_t pad;
+    const void* gfac[2 * kKargGroups];   // per group g: [2g] = A_g, [2g + 1] = B_g
+    float gscale[kKargGroups];           // per group: s_g
 };
+static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 
 // ---------------------------------------------------------------------------
 // Tiling, shared by the planner (sizes the items) and the kernels (lays out

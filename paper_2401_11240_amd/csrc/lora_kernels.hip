@@ -28,8 +28,23 @@
 // a multiple of 16 inside LDS and registers only), so items of different
 // ranks share one grid; the bodies are compiled for the number of rank tiles
 // (or column tiles) per wave and of 16-row subtiles, so the MFMA loops have no
-// branches.  No workgroup waits for another: results are independent of
-// scheduling and bit-reproducible.
+// branches.
+//
+// Step launch: one grid holds every shrink item, then every expand item.  Its
+// partial blocks live in a buffer of their own that holds a sentinel bit
+// pattern between launches.  A shrink workgroup writes its block with
+// device-coherent stores (the L2 caches of the XCDs are not coherent with each
+// other; these stores write through to the common level instead of flushing a
+// cache).  An expand workgroup requests its B tile and its y values, stages
+// B^T, then loads the partial values it needs with device-coherent loads and
+// loads again those that still hold the sentinel: the data is its own ready
+// flag, so no counter or fence sits between a shrink and the expands that use
+// it.  A workgroup only waits for workgroups earlier in the grid, which do not
+// wait, so every wait ends; the number of rounds is bounded all the same (past
+// it the wait gives up and sets the status flag).  The last of a row block's
+// expand items to finish arms the row block's partial blocks again.  The
+// blocks are added in the same fixed order as in the two-launch form, so both
+// give bit-identical results whatever the timing.
 #include <hip/hip_runtime.h>
 
 #include "lora_internal.h"
@@ -87,7 +102,7 @@ struct FmtBF16 {
 // never copied as one aggregate, which would send it to scratch memory).
 struct Item {
     int64_t part;
-    int kind, group, adapter, rank, nrows, lo, len, sub, nsplit, p0, pstride;
+    int kind, group, adapter, rank, nrows, lo, len, sub, nsplit, p0, pstride, rb, nexp;
     int rows[kInlineRows];
 };
 
@@ -105,6 +120,8 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     it.nsplit = p->nsplit;
     it.p0 = p->p0;
     it.pstride = p->pstride;
+    it.rb = p->rb;
+    it.nexp = p->nexp;
 #pragma unroll
     for (int q = 0; q < kInlineRows; ++q) it.rows[q] = p->rows[q];
     return it;
@@ -113,15 +130,28 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
 __device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xffffu; }
 __device__ __forceinline__ uint32_t hi16(uint32_t w) { return w >> 16; }
 
-// The factor this item streams and the group's scale: from the launch's
-// argument table, or from the device registry for groups beyond it.
+// Where the factor pointers and scales of a launch's groups are read.
+enum : int {
+    kLookupAuto = 0,     // the argument table for groups below kKargGroups, else the registry
+    kLookupArgs = 1,     // the argument table only (the launch has at most kKargGroups groups)
+    kLookupReg = 2,      // the device registry only
+};
+
+// The factor this item streams and the group's scale.  The step kernel fixes
+// the source at compile time: a pointer that could point into either the
+// kernel arguments or the registry makes the compiler copy the arguments to
+// private memory.
+template <int kLookup>
 __device__ __forceinline__ gu16* item_factor(const KernelArgs& a, const Item& it, bool shrink) {
-    if (it.group < kKargGroups) return (gu16*)a.gptr[it.group];
+    if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups))
+        return (gu16*)a.gfac[2 * it.group + (shrink ? 0 : 1)];
     const DevAdapter* d = a.table + it.adapter;
     return (gu16*)(shrink ? d->A : d->B);
 }
+template <int kLookup>
 __device__ __forceinline__ float item_scale(const KernelArgs& a, const Item& it) {
-    if (it.group < kKargGroups) return a.gscale[it.group];
+    if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups))
+        return a.gscale[it.group];
     return a.table[it.adapter].scale;
 }
 
@@ -151,17 +181,91 @@ __device__ __forceinline__ int row_of(int rowv, int r) {
     return __builtin_amdgcn_ds_bpermute(r << 2, rowv);
 }
 
-// Part q of the ordered sum of a row block's partial blocks at one position:
-// blocks q, q+P, q+2P, ... added in that order, eight loads in flight.
-__device__ __forceinline__ float part_sum(const float* src, int64_t pstride, int nsplit, int P,
-                                          int q, bool ok) {
+// Partial-block stores and loads: plain, or device-coherent (agent scope) in
+// the step launch, where producer and consumer may sit on different XCDs.
+template <bool kSync>
+__device__ __forceinline__ void put_f32(float* p, float v) {
+    if constexpr (kSync) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else *p = v;
+}
+template <bool kSync>
+__device__ __forceinline__ void put_f32x4(float* p, const f32x4& v) {   // p 16-byte aligned
+    if constexpr (kSync) {
+        const uint64_t lo = (uint64_t)__float_as_uint(v[0]) | ((uint64_t)__float_as_uint(v[1]) << 32);
+        const uint64_t hi = (uint64_t)__float_as_uint(v[2]) | ((uint64_t)__float_as_uint(v[3]) << 32);
+        __hip_atomic_store((uint64_t*)p, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store((uint64_t*)p + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+        *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+    }
+}
+template <bool kSync>
+__device__ __forceinline__ float get_f32(const float* p) {
+    if constexpr (kSync) return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else return *p;
+}
+
+// Step launch: between launches the partial blocks hold this bit pattern, a
+// NaN whose low payload bits no 16-bit input can carry into a float32 sum.
+constexpr uint32_t kSentinel = 0xffffffffu;
+__device__ __forceinline__ bool unready(float v) { return __float_as_uint(v) == kSentinel; }
+
+// Part q of the ordered sums of a row block's partial blocks at two positions
+// (two consecutive ranks): blocks q, q+P, q+2P, ... added in that order,
+// sixteen loads in flight.  In the step launch a value that still holds the
+// sentinel has not been written yet and is loaded again; budget is the
+// thread's remaining polling rounds (spin_limit for the whole item): once it
+// is spent the status flag is raised and values are used as they are.
+template <bool kSync>
+__device__ __forceinline__ float2 part_sum2(const KernelArgs& a, const float* src0, const float* src1,
+                                            int64_t pstride, int nsplit, int P, int q, bool ok0, bool ok1,
+                                            int& budget) {
+    float s0 = 0.f, s1 = 0.f;
+    for (int c0 = q; c0 < nsplit; c0 += 8 * P) {
+        float u[8], w[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int c = c0 + i * P;
+            const int64_t off = (int64_t)c * pstride;
+            u[i] = (ok0 && c < nsplit) ? get_f32<kSync>(src0 + off) : 0.f;
+            w[i] = (ok1 && c < nsplit) ? get_f32<kSync>(src1 + off) : 0.f;
+        }
+        if constexpr (kSync) {
+            for (;;) {
+                bool miss = false;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) miss |= unready(u[i]) | unready(w[i]);
+                if (!miss || budget < 0) break;
+                if (budget-- == 0) {
+                    __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {     // only positions that were loaded can hold the sentinel
+                    const int64_t off = (int64_t)(c0 + i * P) * pstride;
+                    if (unready(u[i])) u[i] = get_f32<true>(src0 + off);
+                    if (unready(w[i])) w[i] = get_f32<true>(src1 + off);
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s0 += u[i];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s1 += w[i];
+    }
+    return make_float2(s0, s1);
+}
+
+// The same ordered sum at one position (the reduce kernel's).
+__device__ __forceinline__ float part_sum(const float* src, int64_t pstride, int nsplit, int P, int q) {
     float s = 0.f;
     for (int c0 = q; c0 < nsplit; c0 += 8 * P) {
         float u[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int c = c0 + i * P;
-            u[i] = (ok && c < nsplit) ? src[(int64_t)c * pstride] : 0.f;
+            u[i] = c < nsplit ? src[(int64_t)c * pstride] : 0.f;
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) s += u[i];
@@ -169,10 +273,27 @@ __device__ __forceinline__ float part_sum(const float* src, int64_t pstride, int
     return s;
 }
 
+// Step launch, end of an expand item: the last of the row block's expand
+// items to finish (its departure count dep + 1 == nexp) arms the row block's
+// partial blocks again and clears its counter, for the next launch.  flag is
+// LDS that no thread reads any more.
+__device__ __forceinline__ void rearm_row_block(const KernelArgs& a, const Item& it, uint32_t dep,
+                                                int* flag) {
+    if (threadIdx.x == 0) *flag = dep + 1 == (uint32_t)it.nexp;
+    __syncthreads();
+    if (*flag) {
+        uint32_t* p = (uint32_t*)(a.partials + it.part);
+        const int n = it.nsplit * it.pstride;
+        for (int i = threadIdx.x; i < n; i += kThreads)
+            __hip_atomic_store(p + i, kSentinel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (threadIdx.x == 0) __hip_atomic_store(a.sync + it.rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Shrink
 // ---------------------------------------------------------------------------
-template <class Fmt, int TQ, int MS>
+template <class Fmt, int TQ, int MS, bool kSync, int kLookup>
 __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
                                             unsigned char* smem) {
     const int t = threadIdx.x;
@@ -192,7 +313,7 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     const int wk = w / WN;
     uint32_t* As = (uint32_t*)smem;                               // [Rp][KP] words
     uint16_t* Xs = (uint16_t*)(smem + (size_t)Rp * KP * 4);       // [MS*16][KX]
-    gu16* A = item_factor(a, it, true) + (int64_t)it.lo * R;
+    gu16* A = item_factor<kLookup>(a, it, true) + (int64_t)it.lo * R;
     const uint16_t* X = (const uint16_t*)a.x + it.lo;
     const int rowv = lane_rows(a, it);
     const u32x4 z4 = {0u, 0u, 0u, 0u};
@@ -325,11 +446,11 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
                     const int r0 = tile * 16 + 4 * lg;
                     float* dst = part + row * R + r0;
                     if ((R & 3) == 0 && r0 + 3 < R) {
-                        *(float4*)dst = make_float4(acc[m][q][0], acc[m][q][1], acc[m][q][2], acc[m][q][3]);
+                        put_f32x4<kSync>(dst, acc[m][q]);
                     } else {
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
-                            if (r0 + i < R) dst[i] = acc[m][q][i];
+                            if (r0 + i < R) put_f32<kSync>(dst + i, acc[m][q][i]);
                     }
                 }
             }
@@ -353,37 +474,44 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
             const int rank = o - row * R;
             float s = red[row * Rp + rank];
             for (int k = 1; k < WK; ++k) s += red[(k * MS * 16 + row) * Rp + rank];
-            part[o] = s;
+            put_f32<kSync>(part + o, s);
         }
     }
 }
 
-template <class Fmt>
-__global__ void __launch_bounds__(kThreads) lora_shrink_kernel(KernelArgs a) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[kShrinkLds];
-    const Item it = load_item(a.items + blockIdx.x);
-    if (it.kind != kItemShrink) return;
+template <class Fmt, bool kSync, int kLookup>
+__device__ __forceinline__ void shrink_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
     const int tq = shrink_tq(it.rank);
     const int ms = msub_body(it.nrows);
     if (tq == 1) {
-        if (ms == 1) shrink_body<Fmt, 1, 1>(a, it, smem);
-        else if (ms == 2) shrink_body<Fmt, 1, 2>(a, it, smem);
-        else shrink_body<Fmt, 1, 4>(a, it, smem);
+        if (ms == 1) shrink_body<Fmt, 1, 1, kSync, kLookup>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 1, 2, kSync, kLookup>(a, it, smem);
+        else shrink_body<Fmt, 1, 4, kSync, kLookup>(a, it, smem);
     } else if (tq == 2) {
-        if (ms == 1) shrink_body<Fmt, 2, 1>(a, it, smem);
-        else if (ms == 2) shrink_body<Fmt, 2, 2>(a, it, smem);
-        else shrink_body<Fmt, 2, 4>(a, it, smem);
+        if (ms == 1) shrink_body<Fmt, 2, 1, kSync, kLookup>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 2, 2, kSync, kLookup>(a, it, smem);
+        else shrink_body<Fmt, 2, 4, kSync, kLookup>(a, it, smem);
     } else {
-        if (ms == 1) shrink_body<Fmt, 4, 1>(a, it, smem);
-        else if (ms == 2) shrink_body<Fmt, 4, 2>(a, it, smem);
-        else shrink_body<Fmt, 4, 4>(a, it, smem);
+        if (ms == 1) shrink_body<Fmt, 4, 1, kSync, kLookup>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 4, 2, kSync, kLookup>(a, it, smem);
+        else shrink_body<Fmt, 4, 4, kSync, kLookup>(a, it, smem);
     }
+}
+
+// Two workgroups per CU: the register budget is capped at 256 per lane.
+template <class Fmt>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+lora_shrink_kernel(KernelArgs a) {
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kShrinkLds];
+    const Item it = load_item(a.items + blockIdx.x);
+    if (it.kind != kItemShrink) return;
+    shrink_item<Fmt, false, kLookupAuto>(a, it, smem);
 }
 
 // ---------------------------------------------------------------------------
 // Expand
 // ---------------------------------------------------------------------------
-template <class Fmt, int Q, int MS>
+template <class Fmt, int Q, int MS, bool kSync, int kLookup>
 __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                                             unsigned char* smem) {
     const int t = threadIdx.x;
@@ -403,8 +531,8 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     uint32_t* Vh = Bs + ncol * RP;            // [MS*16][RP]  high part of v
     uint32_t* Vl = Vh + MS * 16 * RP;         // [MS*16][RP]  low part of v
     float2* red = (float2*)(Vl + MS * 16 * RP);   // [kThreads]
-    gu16* B = item_factor(a, it, false);
-    const float scale = item_scale(a, it);
+    gu16* B = item_factor<kLookup>(a, it, false);
+    const float scale = item_scale<kLookup>(a, it);
     const int rowv = lane_rows(a, it);
     const u32x4 z4 = {0u, 0u, 0u, 0u};
 
@@ -450,36 +578,48 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     const int nslot = MS * 16 * half;
     const int P = a.v ? 1 : partial_parts(nrows, R, it.nsplit);
     const float* Pb = a.partials + it.part;
-    if (P > 1) {
-        const int slot = t % slots;
-        const int q = t / slots;
-        if (q < P) {
-            const int row = slot / half;
-            const int j = 2 * (slot - row * half);
-            const float* src = Pb + row * R;
-            const float s0 = part_sum(src + (j < R ? j : 0), it.pstride, it.nsplit, P, q, j < R);
-            const float s1 = part_sum(src + (j + 1 < R ? j + 1 : 0), it.pstride, it.nsplit, P, q, j + 1 < R);
-            red[t] = make_float2(s0, s1);
+    int budget = a.spin_limit;                // step launch: polling rounds left to this thread
+    auto sum_parts = [&]() {
+        if (P > 1) {
+            const int slot = t % slots;
+            const int q = t / slots;
+            if (q < P) {
+                const int row = slot / half;
+                const int j = 2 * (slot - row * half);
+                const float* src = Pb + row * R;
+                red[t] = part_sum2<kSync>(a, src + (j < R ? j : 0), src + (j + 1 < R ? j + 1 : 0), it.pstride,
+                                          it.nsplit, P, q, j < R, j + 1 < R, budget);
+            }
         }
-    }
-
+    };
     // --- B^T to LDS
+    auto store_bt = [&]() {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int p = t + i * kThreads;
-        if (p < npairs) {
-            const int jp = p / cv;
-            const int co = p - jp * cv;
-            uint32_t* d = Bs + (co * 8) * RP + jp;
-            d[0 * RP] = lo16(b0[i].x) | (b1[i].x << 16);
-            d[1 * RP] = hi16(b0[i].x) | (b1[i].x & 0xffff0000u);
-            d[2 * RP] = lo16(b0[i].y) | (b1[i].y << 16);
-            d[3 * RP] = hi16(b0[i].y) | (b1[i].y & 0xffff0000u);
-            d[4 * RP] = lo16(b0[i].z) | (b1[i].z << 16);
-            d[5 * RP] = hi16(b0[i].z) | (b1[i].z & 0xffff0000u);
-            d[6 * RP] = lo16(b0[i].w) | (b1[i].w << 16);
-            d[7 * RP] = hi16(b0[i].w) | (b1[i].w & 0xffff0000u);
+        for (int i = 0; i < 4; ++i) {
+            const int p = t + i * kThreads;
+            if (p < npairs) {
+                const int jp = p / cv;
+                const int co = p - jp * cv;
+                uint32_t* d = Bs + (co * 8) * RP + jp;
+                d[0 * RP] = lo16(b0[i].x) | (b1[i].x << 16);
+                d[1 * RP] = hi16(b0[i].x) | (b1[i].x & 0xffff0000u);
+                d[2 * RP] = lo16(b0[i].y) | (b1[i].y << 16);
+                d[3 * RP] = hi16(b0[i].y) | (b1[i].y & 0xffff0000u);
+                d[4 * RP] = lo16(b0[i].z) | (b1[i].z << 16);
+                d[5 * RP] = hi16(b0[i].z) | (b1[i].z & 0xffff0000u);
+                d[6 * RP] = lo16(b0[i].w) | (b1[i].w << 16);
+                d[7 * RP] = hi16(b0[i].w) | (b1[i].w & 0xffff0000u);
+            }
         }
+    };
+    if constexpr (kSync) {
+        // the B tile and y are requested and B^T staged before the partial
+        // blocks are polled
+        store_bt();
+        sum_parts();
+    } else {
+        sum_parts();
+        store_bt();
     }
     if (P > 1) __syncthreads();               // the P-way sums are in red
     // --- v to LDS as high / low 16-bit parts (rows past nrows: zero)
@@ -501,8 +641,10 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                 }
             } else {
                 const float* src = Pb + row * R;
-                v0 += part_sum(src + (j < R ? j : 0), it.pstride, it.nsplit, 1, 0, j < R);
-                v1 += part_sum(src + (j + 1 < R ? j + 1 : 0), it.pstride, it.nsplit, 1, 0, j + 1 < R);
+                const float2 s2 = part_sum2<kSync>(a, src + (j < R ? j : 0), src + (j + 1 < R ? j + 1 : 0),
+                                                   it.pstride, it.nsplit, 1, 0, j < R, j + 1 < R, budget);
+                v0 += s2.x;
+                v1 += s2.y;
             }
         }
         const uint32_t h0 = Fmt::from_f32(v0), h1 = Fmt::from_f32(v1);
@@ -512,6 +654,9 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         Vl[row * RP + jp] = l0 | (l1 << 16);
     }
     __syncthreads();
+    uint32_t dep = 0;   // step launch: this item's place among the row block's departures
+    if constexpr (kSync)
+        if (t == 0) dep = __hip_atomic_fetch_add(a.sync + it.rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
     // --- y^T = B^T v^T on MFMA, then y + s*d rounded once
     f32x4 acc[Q][MS];
@@ -555,6 +700,28 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             }
         }
     }
+    if constexpr (kSync) rearm_row_block(a, it, dep, (int*)red);
+}
+
+template <class Fmt, bool kSync, int kLookup>
+__device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
+    const int q = (round_up_i(it.len, 16) / 16 + 3) / 4;   // column tiles per wave
+    const int ms = msub_body(it.nrows);
+    if (ms == 1) {
+        if (q <= 1) expand_body<Fmt, 1, 1, kSync, kLookup>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 1, kSync, kLookup>(a, it, smem);
+        else if (q <= 4) expand_body<Fmt, 4, 1, kSync, kLookup>(a, it, smem);
+        else expand_body<Fmt, 8, 1, kSync, kLookup>(a, it, smem);
+    } else if (ms == 2) {
+        if (q <= 1) expand_body<Fmt, 1, 2, kSync, kLookup>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 2, kSync, kLookup>(a, it, smem);
+        else if (q <= 4) expand_body<Fmt, 4, 2, kSync, kLookup>(a, it, smem);
+        else expand_body<Fmt, 8, 2, kSync, kLookup>(a, it, smem);
+    } else {
+        if (q <= 1) expand_body<Fmt, 1, 4, kSync, kLookup>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 4, kSync, kLookup>(a, it, smem);
+        else expand_body<Fmt, 4, 4, kSync, kLookup>(a, it, smem);
+    }
 }
 
 template <class Fmt>
@@ -562,23 +729,19 @@ __global__ void __launch_bounds__(kThreads) lora_expand_kernel(KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLds];
     const Item it = load_item(a.items + blockIdx.x);
     if (it.kind != kItemExpand) return;
-    const int q = (round_up_i(it.len, 16) / 16 + 3) / 4;   // column tiles per wave
-    const int ms = msub_body(it.nrows);
-    if (ms == 1) {
-        if (q <= 1) expand_body<Fmt, 1, 1>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 1>(a, it, smem);
-        else if (q <= 4) expand_body<Fmt, 4, 1>(a, it, smem);
-        else expand_body<Fmt, 8, 1>(a, it, smem);
-    } else if (ms == 2) {
-        if (q <= 1) expand_body<Fmt, 1, 2>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 2>(a, it, smem);
-        else if (q <= 4) expand_body<Fmt, 4, 2>(a, it, smem);
-        else expand_body<Fmt, 8, 2>(a, it, smem);
-    } else {
-        if (q <= 1) expand_body<Fmt, 1, 4>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 4>(a, it, smem);
-        else expand_body<Fmt, 4, 4>(a, it, smem);
-    }
+    expand_item<Fmt, false, kLookupAuto>(a, it, smem);
+}
+
+// ---------------------------------------------------------------------------
+// Step: shrink items, then expand items, in one grid (two workgroups per CU).
+// ---------------------------------------------------------------------------
+template <class Fmt, int kLookup>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+lora_step_kernel(KernelArgs a) {
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kStepLds];
+    const Item it = load_item(a.items + blockIdx.x);
+    if (it.kind == kItemShrink) shrink_item<Fmt, true, kLookup>(a, it, smem);
+    else if (it.kind == kItemExpand) expand_item<Fmt, true, kLookup>(a, it, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -594,7 +757,7 @@ __global__ void __launch_bounds__(kThreads) lora_reduce_kernel(KernelArgs a) {
     const int P = partial_parts(it.nrows, R, it.nsplit);   // the expand's order
     for (int o = threadIdx.x; o < n; o += kThreads) {
         float s = 0.f;
-        for (int q = 0; q < P; ++q) s += part_sum(Pb + o, it.pstride, it.nsplit, P, q, true);
+        for (int q = 0; q < P; ++q) s += part_sum(Pb + o, it.pstride, it.nsplit, P, q);
         const int i = o / R;
         a.v[(int64_t)a.perm[it.p0 + i] * a.ldv + (o - i * R)] = s;
     }
@@ -618,6 +781,20 @@ hipError_t launch_expand(const KernelArgs& a, int dtype, hipStream_t s) {
         hipLaunchKernelGGL(lora_expand_kernel<FmtF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
     else
         hipLaunchKernelGGL(lora_expand_kernel<FmtBF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_step(const KernelArgs& a, int dtype, hipStream_t s) {
+    if (a.n_items <= 0) return hipSuccess;
+    const dim3 g(a.n_items), b(kThreads);
+    const bool args = a.n_groups <= kKargGroups;
+    if (dtype == 0) {
+        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupArgs>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupReg>), g, b, 0, s, a);
+    } else {
+        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupArgs>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupReg>), g, b, 0, s, a);
+    }
     return hipGetLastError();
 }
 

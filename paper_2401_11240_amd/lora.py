@@ -30,13 +30,14 @@ LORA_E_NOMEM = -6
 LORA_E_HIP = -7
 LORA_E_WORKSPACE = -8
 LORA_E_OVERLAP = -9
+LORA_E_SYNC = -10
 
 # Every function the header declares (checked by the tests).
 EXPORTS = (
     "lora_register_adapters", "lora_release_adapters", "lora_workspace_bytes", "lora_shrink",
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
-    "lora_plan_shrink", "lora_plan_expand", "lora_group_rows", "lora_last_error",
-    "lora_abi_version",
+    "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
+    "lora_group_rows", "lora_last_error", "lora_abi_version",
 )
 
 
@@ -102,6 +103,8 @@ def load():
         "lora_plan_destroy": [vp],
         "lora_plan_shrink": [vp, vp, vp, i64, vp],
         "lora_plan_expand": [vp, vp, vp, i64, vp],
+        "lora_plan_status": [vp, vp],
+        "lora_plan_set_spin_limit": [vp, i32],
         "lora_group_rows": [C.POINTER(_Batch), i32, i32p, i32p, i32p, i32p],
         "lora_last_error": [],
         "lora_abi_version": [],
@@ -208,6 +211,15 @@ def lora_plan_expand(plan: int, table, y, ldy: int, stream=None) -> None:
 
 def lora_plan_destroy(plan: int) -> None:
     _check(load().lora_plan_destroy(plan))
+
+
+def lora_plan_status(plan: int, stream=None) -> None:
+    """Raise LoraError(LORA_E_SYNC) if a step launch of the plan gave up waiting."""
+    _check(load().lora_plan_status(plan, _stream(stream)))
+
+
+def lora_plan_set_spin_limit(plan: int, polls: int) -> None:
+    _check(load().lora_plan_set_spin_limit(plan, int(polls)))
 
 
 def lora_group_rows(batch: Batch, n_adapters: int):

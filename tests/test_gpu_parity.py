@@ -1,9 +1,10 @@
 """HIP path vs the CPU oracle, element by element, through the C ABI.
 
 Small cases compare every output; the five named Llama-shaped workloads run
-at full size in the same launch configuration the benchmark times and are
-checked on sampled rows (the oracle computes rows one by one) plus
-properties that hold at any size.
+at full size through the plan's step launch (the configuration the benchmark
+times), are checked bit for bit against the two-launch form and, on sampled
+rows, against the oracle (which computes rows one by one), plus properties
+that hold at any size.
 """
 import os
 import sys
@@ -50,6 +51,20 @@ def run_fused(dw, name):
     ws, n = workspace(p.table, dw.batch)
     L.lora_apply_fused(p.table, dw.batch, x, x.shape[1], y, y.shape[1], ws, n, stream())
     torch.cuda.synchronize()
+    return D.from_device_bits(y)
+
+
+def run_plan(dw, name):
+    """The plan path (one step launch), as the benchmark runs it."""
+    p = dw.projection(name)
+    x = dw.xs[p.x]
+    y = p.y.clone()
+    plan = L.lora_plan_create(p.table, dw.batch, stream())
+    try:
+        L.lora_plan_apply(plan, None, x, x.shape[1], y, y.shape[1], stream())
+        L.lora_plan_status(plan, stream())
+    finally:
+        L.lora_plan_destroy(plan)
     return D.from_device_bits(y)
 
 
@@ -260,6 +275,79 @@ def test_plan_reuse_and_determinism():
             L.lora_plan_apply(plan, None, x, x.shape[1], y, y.shape[1], stream())
             torch.cuda.synchronize()
             assert np.array_equal(D.from_device_bits(y), ref), rep
+        L.lora_plan_status(plan, stream())
+    finally:
+        L.lora_plan_destroy(plan)
+    dw.release()
+
+
+def test_step_launch_graph_replays():
+    """The step launch captured in a HIP graph: every replay re-arms the row
+    block counters and gives the eager two-launch result bit for bit."""
+    w = random_workload(RANDOM_CASES[1])
+    dw = D.upload(w, DEV)
+    p = dw.projection("proj")
+    x = dw.xs["x"]
+    ref = run_fused(dw, "proj")
+    plan = L.lora_plan_create(p.table, dw.batch, stream())
+    try:
+        y = p.y.clone()
+        side = torch.cuda.Stream(DEV)
+        side.wait_stream(torch.cuda.current_stream(DEV))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                L.lora_plan_apply(plan, None, x, x.shape[1], y, y.shape[1], side)
+        torch.cuda.synchronize()
+        for rep in range(4):
+            y.copy_(p.y)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert np.array_equal(D.from_device_bits(y), ref), rep
+            # eager work between the replays
+            y2 = p.y.clone()
+            L.lora_plan_apply(plan, None, x, x.shape[1], y2, y2.shape[1], stream())
+            torch.cuda.synchronize()
+            assert np.array_equal(D.from_device_bits(y2), ref), rep
+        L.lora_plan_status(plan, stream())
+        del g
+    finally:
+        L.lora_plan_destroy(plan)
+    dw.release()
+
+
+def test_step_wait_that_gives_up_is_reported_and_recovered():
+    """A spin limit of zero (set from the host) makes every expand workgroup
+    give up at once: the launch still ends, the status reports LORA_E_SYNC and
+    resets the counters, and the next launch with the normal limit is exact."""
+    w = random_workload(RANDOM_CASES[1])
+    dw = D.upload(w, DEV)
+    p = dw.projection("proj")
+    x = dw.xs["x"]
+    ref = run_fused(dw, "proj")
+    plan = L.lora_plan_create(p.table, dw.batch, stream())
+    try:
+        L.lora_plan_set_spin_limit(plan, 0)
+        y = p.y.clone()
+        L.lora_plan_apply(plan, None, x, x.shape[1], y, y.shape[1], stream())
+        torch.cuda.synchronize()
+        gave_up = False
+        try:
+            L.lora_plan_status(plan, stream())
+        except L.LoraError as e:
+            assert e.code == L.LORA_E_SYNC
+            gave_up = True
+        say(f"  spin limit 0: wait gave up = {gave_up}")
+        L.lora_plan_status(plan, stream())          # cleared
+        L.lora_plan_set_spin_limit(plan, 1 << 18)
+        y = p.y.clone()
+        L.lora_plan_apply(plan, None, x, x.shape[1], y, y.shape[1], stream())
+        L.lora_plan_status(plan, stream())
+        assert np.array_equal(D.from_device_bits(y), ref)
+        with pytest.raises(L.LoraError) as e:
+            L.lora_plan_set_spin_limit(plan, -1)
+        assert e.value.code == L.LORA_E_ARG
     finally:
         L.lora_plan_destroy(plan)
     dw.release()
@@ -398,7 +486,8 @@ def test_named_workload_full_size(name):
     dw = D.upload(w, DEV)
     say(f"  uploaded, T={w.n_rows}")
     for p in w.projections:
-        got = run_fused(dw, p.name)
+        got = run_plan(dw, p.name)
+        assert np.array_equal(got, run_fused(dw, p.name))   # one step launch == two launches
         if w.n_rows <= 64:
             ref = oracle_full(w, p.name)
             st = compare(got, ref, w.dtype, f"{name}/{p.name}")
