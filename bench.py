@@ -38,6 +38,19 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, datasheet
+
+# HBM traffic of one step launch of the headline workload, from two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) scaled by the
+# same counters on a plain 256 MiB device copy in the same run (FETCH_SIZE
+# reads 131,091.9 KiB for 262,144 KiB read: x 1.99970; WRITE_SIZE reads
+# 262,144.0 KiB: x 1.0).  Valid only for the kernel sources it was taken on
+# (hash of csrc/*); reported as null otherwise.
+MEASURED_TRAFFIC = {
+    "sources_sha256_16": "354ae6359b1b71ef",
+    "workload": "decode_q4096_t64_mixed_rank_f16",
+    "fetch_kib": 7301.4, "fetch_scale": 262144.0 / 131091.9,
+    "write_kib": 780.2, "write_scale": 1.0,
+}
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16
 METRIC = "LoRA-delta HBM GB/s (% peak) at decode b=64 mixed rank; prefill tokens/s"
 
@@ -58,6 +71,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=float, default=0.0,
+                    help="also run one plain device copy of this many MiB (a known-traffic kernel "
+                         "for scaling hardware byte counters)")
     return ap.parse_args()
 
 
@@ -181,6 +197,24 @@ def measure(torch, w, dev, steps, warmup, rotate_mib, label):
     )
 
 
+def sources_hash() -> str:
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2401_11240_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("lora_api.hip", "lora_internal.h", "lora_kernels.hip"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per step launch from the counters, if they describe these sources."""
+    m = MEASURED_TRAFFIC
+    if m["workload"] != workload_name or m["sources_sha256_16"] != sources_hash():
+        return None
+    return int(round((m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024))
+
+
 def cpu_baseline(w, seconds):
     import oracle
     from paper_2401_11240_amd import workloads as W
@@ -257,7 +291,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(w.name),
             "avg_launch_us": round(step_us, 3),
             "algorithmic_bytes_per_launch": step_bytes,
         },
@@ -286,6 +320,15 @@ def main():
             "algorithmic_bytes_per_step": pre["bytes_per_step"],
             "rotated_copies": pre["R"],
         }
+    if args.calibrate_copy_mib > 0:
+        n = int(args.calibrate_copy_mib * 2 ** 20)
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = {"read": n, "write": n}
+        del src, dst
     if not args.no_cpu_baseline:
         log("[cpu] timing the oracle")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

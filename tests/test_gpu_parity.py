@@ -317,6 +317,57 @@ def test_step_launch_graph_replays():
     dw.release()
 
 
+def test_step_launch_alternating_layers():
+    """Consecutive step launches of one plan on different layers (tables and
+    inputs): a partial value left over from the previous launch would give
+    that layer's numbers, so every launch is checked against its own
+    two-launch result, eagerly and inside one captured graph."""
+    c = RANDOM_CASES[1]
+    w1 = random_workload(c)
+    w2 = W.build_workload(name="layer2", seed=78, dtype=w1.dtype, n_adapters=w1.n_adapters,
+                          fixed_ranks=w1.ranks, seg_adapter=w1.seg_adapter,
+                          seg_lens=np.diff(w1.seg_offset), projections=(("proj", c[2], c[3], "x"),))
+    d1, d2 = D.upload(w1, DEV), D.upload(w2, DEV)
+    ref = [run_fused(d1, "proj"), run_fused(d2, "proj")]
+    layers = [(d1.projection("proj"), d1.xs["x"]), (d2.projection("proj"), d2.xs["x"])]
+    plan = L.lora_plan_create(layers[0][0].table, d1.batch, stream())
+    try:
+        for rep in range(3):
+            for i, (p, x) in enumerate(layers):
+                y = p.y.clone()
+                L.lora_plan_apply(plan, p.table, x, x.shape[1], y, y.shape[1], stream())
+                torch.cuda.synchronize()
+                assert np.array_equal(D.from_device_bits(y), ref[i]), (rep, i)
+        ys = [p.y.clone() for p, _ in layers]
+        side = torch.cuda.Stream(DEV)
+        side.wait_stream(torch.cuda.current_stream(DEV))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(g, stream=side):
+                for k in range(4):   # layer 1, 2, 1, 2: the last two redo the first two on their output
+                    p, x = layers[k % 2]
+                    L.lora_plan_apply(plan, p.table, x, x.shape[1], ys[k % 2], ys[k % 2].shape[1], side)
+        torch.cuda.synchronize()
+        for rep in range(3):
+            for i, (p, _) in enumerate(layers):
+                ys[i].copy_(p.y)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for i, (p, x) in enumerate(layers):
+                # twice applied: the second launch adds the delta once more onto the first result
+                y = torch.from_numpy(ref[i].view(np.int16)).to(DEV)
+                L.lora_plan_apply(plan, p.table, x, x.shape[1], y, y.shape[1], stream())
+                torch.cuda.synchronize()
+                assert np.array_equal(D.from_device_bits(ys[i]), D.from_device_bits(y)), (rep, i)
+        L.lora_plan_status(plan, stream())
+        del g
+    finally:
+        L.lora_plan_destroy(plan)
+    d1.release()
+    d2.release()
+
+
 def test_step_wait_that_gives_up_is_reported_and_recovered():
     """A spin limit of zero (set from the host) makes every expand workgroup
     give up at once: the launch still ends, the status reports LORA_E_SYNC and
