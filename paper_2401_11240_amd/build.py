@@ -18,8 +18,11 @@ SOURCES = ["lora_api.hip", "lora_kernels.hip"]
 ARCH = "gfx950"
 
 # Packed-FP32 VALU forms are kept out of the device code; the host pass warns
-# that it does not know the feature, which is harmless.
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# that it does not know the feature, which is harmless.  The first kernel
+# argument (the step kernel's item list, 8 bytes) is preloaded into scalar
+# registers at wave launch instead of being read from the argument segment.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-kernarg-preload-count=2"]
 
 
 def hipcc() -> str:

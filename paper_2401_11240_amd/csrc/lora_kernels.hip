@@ -46,6 +46,7 @@
 // blocks are added in the same fixed order as in the two-launch form, so both
 // give bit-identical results whatever the timing.
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 
 #include "lora_internal.h"
 
@@ -104,26 +105,34 @@ struct Item {
     int64_t part;
     int kind, group, adapter, rank, nrows, lo, len, sub, nsplit, p0, pstride, rb, nexp;
     int rows[kInlineRows];
+    const void* fac;     // the factor this item streams: A_g (shrink) or B_g (expand)
+    float scale;         // s_g
 };
 
+// The item's two 64-byte halves are requested together (two scalar loads in
+// flight), so its inline rows cost no second round trip.
+typedef unsigned int u32x16 __attribute__((ext_vector_type(16)));
+static_assert(offsetof(DevItem, rows) == 64 && offsetof(DevItem, nexp) == 56, "DevItem halves");
 __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
+    const u32x16 w0 = ((const u32x16*)p)[0];
+    const u32x16 w1 = ((const u32x16*)p)[1];
     Item it;
-    it.part = p->part;
-    it.kind = p->kind;
-    it.group = p->group;
-    it.adapter = p->adapter;
-    it.rank = p->rank;
-    it.nrows = p->nrows;
-    it.lo = p->lo;
-    it.len = p->len;
-    it.sub = p->sub;
-    it.nsplit = p->nsplit;
-    it.p0 = p->p0;
-    it.pstride = p->pstride;
-    it.rb = p->rb;
-    it.nexp = p->nexp;
+    it.part = (int64_t)(((uint64_t)w0[1] << 32) | w0[0]);
+    it.kind = (int)w0[2];
+    it.group = (int)w0[3];
+    it.adapter = (int)w0[4];
+    it.rank = (int)w0[5];
+    it.nrows = (int)w0[6];
+    it.lo = (int)w0[7];
+    it.len = (int)w0[8];
+    it.sub = (int)w0[9];
+    it.nsplit = (int)w0[10];
+    it.p0 = (int)w0[11];
+    it.pstride = (int)w0[12];
+    it.rb = (int)w0[13];
+    it.nexp = (int)w0[14];
 #pragma unroll
-    for (int q = 0; q < kInlineRows; ++q) it.rows[q] = p->rows[q];
+    for (int q = 0; q < kInlineRows; ++q) it.rows[q] = (int)w1[q];
     return it;
 }
 
@@ -153,6 +162,41 @@ __device__ __forceinline__ float item_scale(const KernelArgs& a, const Item& it)
     if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups))
         return a.gscale[it.group];
     return a.table[it.adapter].scale;
+}
+template <int kLookup>
+__device__ __forceinline__ void resolve(const KernelArgs& a, Item& it) {
+    it.fac = (const void*)item_factor<kLookup>(a, it, it.kind == kItemShrink);
+    it.scale = item_scale<kLookup>(a, it);
+}
+
+// The launch's factor pointers and scales, striped over a wave's lanes: lane
+// l holds gfac[l + 64 i] and gscale[l + 64 i].  Loaded at entry beside the
+// work item, then picked with lane reads, so the pointer costs no second
+// memory round trip after the item arrives.
+struct LaneTable {
+    uint64_t f[4];
+    float s[2];
+};
+static_assert(2 * kKargGroups == 4 * 64 && kKargGroups == 2 * 64, "lane table shape");
+__device__ __forceinline__ LaneTable load_lane_table(const KernelArgs& a) {
+    const int l = threadIdx.x & 63;
+    const uint64_t* g = reinterpret_cast<const uint64_t*>(a.gfac);
+    LaneTable t;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t.f[i] = g[l + 64 * i];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) t.s[i] = a.gscale[l + 64 * i];
+    return t;
+}
+__device__ __forceinline__ void resolve_lanes(const LaneTable& t, Item& it) {
+    const int e = 2 * it.group + (it.kind == kItemShrink ? 0 : 1);   // < 2 * kKargGroups
+    const int slot = e >> 6, lane = e & 63;
+    const uint64_t v = slot == 0 ? t.f[0] : (slot == 1 ? t.f[1] : (slot == 2 ? t.f[2] : t.f[3]));
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+    it.fac = (const void*)(((uint64_t)hi << 32) | lo);
+    const float sv = (it.group >> 6) == 0 ? t.s[0] : t.s[1];
+    it.scale = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sv), it.group & 63));
 }
 
 // v with lane Q replaced by the wave-uniform value s (one VALU lane write).
@@ -293,7 +337,7 @@ __device__ __forceinline__ void rearm_row_block(const KernelArgs& a, const Item&
 // ---------------------------------------------------------------------------
 // Shrink
 // ---------------------------------------------------------------------------
-template <class Fmt, int TQ, int MS, bool kSync, int kLookup>
+template <class Fmt, int TQ, int MS, bool kSync>
 __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
                                             unsigned char* smem) {
     const int t = threadIdx.x;
@@ -313,7 +357,7 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     const int wk = w / WN;
     uint32_t* As = (uint32_t*)smem;                               // [Rp][KP] words
     uint16_t* Xs = (uint16_t*)(smem + (size_t)Rp * KP * 4);       // [MS*16][KX]
-    gu16* A = item_factor<kLookup>(a, it, true) + (int64_t)it.lo * R;
+    gu16* A = (gu16*)it.fac + (int64_t)it.lo * R;
     const uint16_t* X = (const uint16_t*)a.x + it.lo;
     const int rowv = lane_rows(a, it);
     const u32x4 z4 = {0u, 0u, 0u, 0u};
@@ -416,8 +460,10 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
         const int plen = min_i(sub, it.len - pass * sub);
         if (pass + 1 < npass) load_pass(pass + 1);   // in flight during this pass's MFMA
         const int ks = (plen + 31) / 32;
-        for (int s = wk; s < ks; s += WK) {
-            u32x4 af[TQ];
+        // U K-steps per round: every fragment of the round is read from LDS
+        // before its MFMAs, so the reads overlap instead of each MFMA waiting
+        // for its own
+        auto step_frags = [&](int s, u32x4 (&af)[TQ], u32x4 (&xf)[MS]) {
 #pragma unroll
             for (int q = 0; q < TQ; ++q) {
                 const int tile = wn + WN * q;
@@ -426,10 +472,28 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
 #pragma unroll
             for (int m = 0; m < MS; ++m) {
                 const int row = m * 16 + lr;
-                const u32x4 xf = row < nrows ? *(const u32x4*)(Xs + row * KX + 32 * s + 8 * lg) : z4;
-#pragma unroll
-                for (int q = 0; q < TQ; ++q) acc[m][q] = Fmt::mma32(af[q], xf, acc[m][q]);
+                xf[m] = row < nrows ? *(const u32x4*)(Xs + row * KX + 32 * s + 8 * lg) : z4;
             }
+        };
+        auto step_mma = [&](const u32x4 (&af)[TQ], const u32x4 (&xf)[MS]) {
+#pragma unroll
+            for (int m = 0; m < MS; ++m)
+#pragma unroll
+                for (int q = 0; q < TQ; ++q) acc[m][q] = Fmt::mma32(af[q], xf[m], acc[m][q]);
+        };
+        constexpr int U = TQ + MS <= 2 ? 4 : (TQ + MS <= 4 ? 2 : 1);
+        int s = wk;
+        for (; s + (U - 1) * WK < ks; s += U * WK) {
+            u32x4 af[U][TQ], xf[U][MS];
+#pragma unroll
+            for (int u = 0; u < U; ++u) step_frags(s + u * WK, af[u], xf[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) step_mma(af[u], xf[u]);
+        }
+        for (; s < ks; s += WK) {
+            u32x4 af[TQ], xf[MS];
+            step_frags(s, af, xf);
+            step_mma(af, xf);
         }
     }
 
@@ -479,22 +543,22 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     }
 }
 
-template <class Fmt, bool kSync, int kLookup>
+template <class Fmt, bool kSync>
 __device__ __forceinline__ void shrink_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
     const int tq = shrink_tq(it.rank);
     const int ms = msub_body(it.nrows);
     if (tq == 1) {
-        if (ms == 1) shrink_body<Fmt, 1, 1, kSync, kLookup>(a, it, smem);
-        else if (ms == 2) shrink_body<Fmt, 1, 2, kSync, kLookup>(a, it, smem);
-        else shrink_body<Fmt, 1, 4, kSync, kLookup>(a, it, smem);
+        if (ms == 1) shrink_body<Fmt, 1, 1, kSync>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 1, 2, kSync>(a, it, smem);
+        else shrink_body<Fmt, 1, 4, kSync>(a, it, smem);
     } else if (tq == 2) {
-        if (ms == 1) shrink_body<Fmt, 2, 1, kSync, kLookup>(a, it, smem);
-        else if (ms == 2) shrink_body<Fmt, 2, 2, kSync, kLookup>(a, it, smem);
-        else shrink_body<Fmt, 2, 4, kSync, kLookup>(a, it, smem);
+        if (ms == 1) shrink_body<Fmt, 2, 1, kSync>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 2, 2, kSync>(a, it, smem);
+        else shrink_body<Fmt, 2, 4, kSync>(a, it, smem);
     } else {
-        if (ms == 1) shrink_body<Fmt, 4, 1, kSync, kLookup>(a, it, smem);
-        else if (ms == 2) shrink_body<Fmt, 4, 2, kSync, kLookup>(a, it, smem);
-        else shrink_body<Fmt, 4, 4, kSync, kLookup>(a, it, smem);
+        if (ms == 1) shrink_body<Fmt, 4, 1, kSync>(a, it, smem);
+        else if (ms == 2) shrink_body<Fmt, 4, 2, kSync>(a, it, smem);
+        else shrink_body<Fmt, 4, 4, kSync>(a, it, smem);
     }
 }
 
@@ -505,13 +569,15 @@ lora_shrink_kernel(KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kShrinkLds];
     const Item it = load_item(a.items + blockIdx.x);
     if (it.kind != kItemShrink) return;
-    shrink_item<Fmt, false, kLookupAuto>(a, it, smem);
+    Item r = it;
+    resolve<kLookupAuto>(a, r);
+    shrink_item<Fmt, false>(a, r, smem);
 }
 
 // ---------------------------------------------------------------------------
 // Expand
 // ---------------------------------------------------------------------------
-template <class Fmt, int Q, int MS, bool kSync, int kLookup>
+template <class Fmt, int Q, int MS, bool kSync>
 __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                                             unsigned char* smem) {
     const int t = threadIdx.x;
@@ -531,8 +597,8 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     uint32_t* Vh = Bs + ncol * RP;            // [MS*16][RP]  high part of v
     uint32_t* Vl = Vh + MS * 16 * RP;         // [MS*16][RP]  low part of v
     float2* red = (float2*)(Vl + MS * 16 * RP);   // [kThreads]
-    gu16* B = item_factor<kLookup>(a, it, false);
-    const float scale = item_scale<kLookup>(a, it);
+    gu16* B = (gu16*)it.fac;
+    const float scale = it.scale;
     const int rowv = lane_rows(a, it);
     const u32x4 z4 = {0u, 0u, 0u, 0u};
 
@@ -703,24 +769,24 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     if constexpr (kSync) rearm_row_block(a, it, dep, (int*)red);
 }
 
-template <class Fmt, bool kSync, int kLookup>
+template <class Fmt, bool kSync>
 __device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
     const int q = (round_up_i(it.len, 16) / 16 + 3) / 4;   // column tiles per wave
     const int ms = msub_body(it.nrows);
     if (ms == 1) {
-        if (q <= 1) expand_body<Fmt, 1, 1, kSync, kLookup>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 1, kSync, kLookup>(a, it, smem);
-        else if (q <= 4) expand_body<Fmt, 4, 1, kSync, kLookup>(a, it, smem);
-        else expand_body<Fmt, 8, 1, kSync, kLookup>(a, it, smem);
+        if (q <= 1) expand_body<Fmt, 1, 1, kSync>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 1, kSync>(a, it, smem);
+        else if (q <= 4) expand_body<Fmt, 4, 1, kSync>(a, it, smem);
+        else expand_body<Fmt, 8, 1, kSync>(a, it, smem);
     } else if (ms == 2) {
-        if (q <= 1) expand_body<Fmt, 1, 2, kSync, kLookup>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 2, kSync, kLookup>(a, it, smem);
-        else if (q <= 4) expand_body<Fmt, 4, 2, kSync, kLookup>(a, it, smem);
-        else expand_body<Fmt, 8, 2, kSync, kLookup>(a, it, smem);
+        if (q <= 1) expand_body<Fmt, 1, 2, kSync>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 2, kSync>(a, it, smem);
+        else if (q <= 4) expand_body<Fmt, 4, 2, kSync>(a, it, smem);
+        else expand_body<Fmt, 8, 2, kSync>(a, it, smem);
     } else {
-        if (q <= 1) expand_body<Fmt, 1, 4, kSync, kLookup>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 4, kSync, kLookup>(a, it, smem);
-        else expand_body<Fmt, 4, 4, kSync, kLookup>(a, it, smem);
+        if (q <= 1) expand_body<Fmt, 1, 4, kSync>(a, it, smem);
+        else if (q <= 2) expand_body<Fmt, 2, 4, kSync>(a, it, smem);
+        else expand_body<Fmt, 4, 4, kSync>(a, it, smem);
     }
 }
 
@@ -729,19 +795,31 @@ __global__ void __launch_bounds__(kThreads) lora_expand_kernel(KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLds];
     const Item it = load_item(a.items + blockIdx.x);
     if (it.kind != kItemExpand) return;
-    expand_item<Fmt, false, kLookupAuto>(a, it, smem);
+    Item r = it;
+    resolve<kLookupAuto>(a, r);
+    expand_item<Fmt, false>(a, r, smem);
 }
 
 // ---------------------------------------------------------------------------
 // Step: shrink items, then expand items, in one grid (two workgroups per CU).
+// The item list is a kernel argument of its own, ahead of the argument block,
+// so that it can be preloaded into scalar registers at wave launch.
 // ---------------------------------------------------------------------------
 template <class Fmt, int kLookup>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
-lora_step_kernel(KernelArgs a) {
+lora_step_kernel(const DevItem* __restrict__ items, KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kStepLds];
-    const Item it = load_item(a.items + blockIdx.x);
-    if (it.kind == kItemShrink) shrink_item<Fmt, true, kLookup>(a, it, smem);
-    else if (it.kind == kItemExpand) expand_item<Fmt, true, kLookup>(a, it, smem);
+    Item it;
+    if constexpr (kLookup == kLookupArgs) {
+        const LaneTable lt = load_lane_table(a);      // in flight with the item
+        it = load_item(items + blockIdx.x);
+        resolve_lanes(lt, it);
+    } else {
+        it = load_item(items + blockIdx.x);
+        resolve<kLookupReg>(a, it);
+    }
+    if (it.kind == kItemShrink) shrink_item<Fmt, true>(a, it, smem);
+    else if (it.kind == kItemExpand) expand_item<Fmt, true>(a, it, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -789,11 +867,11 @@ hipError_t launch_step(const KernelArgs& a, int dtype, hipStream_t s) {
     const dim3 g(a.n_items), b(kThreads);
     const bool args = a.n_groups <= kKargGroups;
     if (dtype == 0) {
-        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupArgs>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupReg>), g, b, 0, s, a);
+        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupArgs>), g, b, 0, s, a.items, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupReg>), g, b, 0, s, a.items, a);
     } else {
-        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupArgs>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupReg>), g, b, 0, s, a);
+        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupArgs>), g, b, 0, s, a.items, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupReg>), g, b, 0, s, a.items, a);
     }
     return hipGetLastError();
 }
