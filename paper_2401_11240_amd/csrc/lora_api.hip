@@ -247,8 +247,9 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
 
     // device layout: [shrink items][expand items][reduce items][perm] |
     // [partials][row block counters, status] (a workspace ends here) |
-    // [step partials] (plans only: the step launch's partial blocks, armed
-    // with the sentinel between launches).  The expand items follow the shrink
+    // [step partials x 2] (plans only: the step launch's partial blocks in two
+    // buffers used by alternate launches, each armed with the sentinel before
+    // the launch that reads it).  The expand items follow the shrink
     // items directly: the step launch runs both lists as one grid.
     size_t off = 0;
     p.off_shrink = off;
@@ -263,11 +264,11 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.off_partials = off;
     off = align_up(off + (size_t)p.n_partials * sizeof(float));
     p.off_sync = off;
-    p.sync_bytes = align_up(((size_t)p.n_rb + 1) * sizeof(uint32_t));
+    p.sync_bytes = align_up(((size_t)p.n_rb + 1) * kSyncStride * sizeof(uint32_t));
     off += p.sync_bytes;
     p.total_bytes = std::max<size_t>(off, kAlign);
     p.off_step_partials = off;
-    p.step_partials_bytes = align_up((size_t)p.n_partials * sizeof(float));
+    p.step_partials_bytes = 2 * align_up((size_t)p.n_partials * sizeof(float));   // two buffers
     p.plan_total_bytes = std::max<size_t>(off + p.step_partials_bytes, kAlign);
 
     p.blob.assign(p.plan_bytes, 0);
@@ -348,7 +349,8 @@ KernelArgs make_args(const lora_table_s* t, const HostPlan& p, unsigned char* w,
     a.table = t->dev;
     a.partials = (float*)(w + p.off_partials);
     a.sync = (uint32_t*)(w + p.off_sync);
-    a.status = (int32_t*)(a.sync + p.n_rb);
+    a.status = (int32_t*)(a.sync + (size_t)p.n_rb * kSyncStride);
+    a.pbuf = (int64_t)(p.step_partials_bytes / 2 / sizeof(float));
     a.spin_limit = spin_limit;
     a.h_in = t->h_in;
     a.h_out = t->h_out;
@@ -454,8 +456,8 @@ int enqueue_step(const lora_table_s* t, const HostPlan& p, unsigned char* w, con
     return LORA_OK;
 }
 
-// Counters and status to zero, step partial blocks to the sentinel (all-ones
-// bytes).  Plan creation and the status reset only, never inside a launch
+// Counters and status to zero, both step partial buffers to the sentinel
+// (all-ones bytes).  Plan creation and the status reset only, never inside a launch
 // sequence a caller may capture.
 hipError_t arm_step(const HostPlan& p, unsigned char* w, hipStream_t s) {
     hipError_t e = hipMemsetAsync(w + p.off_sync, 0, p.sync_bytes, s);
@@ -711,7 +713,7 @@ int lora_plan_status(lora_plan_t pl, void* stream) {
     hipStream_t s = (hipStream_t)stream;
     const HostPlan& p = pl->plan;
     int32_t flag = 0;
-    LORA_HIP_TRY(hipMemcpyAsync(&flag, pl->dmem + p.off_sync + p.n_rb * sizeof(uint32_t), sizeof(flag),
+    LORA_HIP_TRY(hipMemcpyAsync(&flag, pl->dmem + p.off_sync + (size_t)p.n_rb * kSyncStride * sizeof(uint32_t), sizeof(flag),
                                 hipMemcpyDeviceToHost, s));
     LORA_HIP_TRY(hipStreamSynchronize(s));
     if (flag == 0) return LORA_OK;

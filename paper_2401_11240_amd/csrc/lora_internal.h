@@ -15,9 +15,10 @@
 // so results never depend on timing.  The two run either as two launches (the
 // launch boundary orders them) or as one step launch whose grid holds every
 // shrink item before every expand item: a shrink workgroup writes its block
-// with device-coherent stores into a buffer armed with a sentinel pattern; an
-// expand workgroup requests its B tile and its y values, then loads the
-// partial values, again while any still holds the sentinel.  It only ever
+// with device-coherent stores into a buffer armed with a sentinel pattern
+// (two buffers, used by alternate launches); an expand workgroup requests its
+// B tile and its y values, then loads the partial values, again while any
+// still holds the sentinel.  It only ever
 // waits for workgroups earlier in the grid, which never wait themselves, and
 // the wait is bounded (it gives up and raises a status flag).
 //
@@ -49,6 +50,7 @@ constexpr int kKargGroups = 128;         // groups whose pointers travel in the 
 constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink kernel
 constexpr int kExpandLds = 68 * 1024;    // LDS bytes of the expand kernel
 constexpr int kStepLds = kExpandLds > kShrinkLds ? kExpandLds : kShrinkLds;
+constexpr int kSyncStride = 32;          // 32-bit words between row block counters (one 128-byte line each)
 
 // Item kinds.
 enum : int32_t {
@@ -82,7 +84,7 @@ struct DevItem {
     int32_t nsplit;      // expand / reduce: partial blocks to add
     int32_t p0;          // position of the first row in the grouped row order (perm)
     int32_t pstride;     // floats between consecutive partial blocks of the row block
-    int32_t rb;          // row block index (its departure counter in the step launch)
+    int32_t rb;          // row block index (its counter of finished expand items in the step launch)
     int32_t nexp;        // expand items of the row block
     int32_t pad;
     int32_t rows[kInlineRows];   // the item's rows when nrows <= kInlineRows
@@ -104,8 +106,9 @@ struct KernelArgs {
     int32_t h_out;
     int32_t n_items;
     int32_t n_groups;
-    uint32_t* sync;             // step launch: per row block, expand items done; zero between launches
+    uint32_t* sync;             // step launch: per row block (every kSyncStride words), expand items finished (wraps at 2 nexp)
     int32_t* status;            // step launch: set to 1 when a wait gave up
+    int64_t pbuf;               // step launch: floats from the first partial buffer to the second
     int32_t spin_limit;         // step launch: polling rounds before a wait gives up
     int32_t pad;
     const void* gfac[2 * kKargGroups];   // per group g: [2g] = A_g, [2g + 1] = B_g

@@ -31,19 +31,18 @@
 // branches.
 //
 // Step launch: one grid holds every shrink item, then every expand item.  Its
-// partial blocks live in a buffer of their own that holds a sentinel bit
-// pattern between launches.  A shrink workgroup writes its block with
-// device-coherent stores (the L2 caches of the XCDs are not coherent with each
-// other; these stores write through to the common level instead of flushing a
-// cache).  An expand workgroup requests its B tile and its y values, stages
+// partial blocks live in two buffers of their own, used by alternate
+// launches; the one a launch reads holds a sentinel bit pattern until it is
+// written.  A shrink workgroup writes its block with device-coherent stores
+// (the L2 caches of the XCDs are not coherent with each other; these stores
+// write through to the common level instead of flushing a cache) and arms its
+// block in the other buffer for the next launch.  An expand workgroup requests its B tile and its y values, stages
 // B^T, then loads the partial values it needs with device-coherent loads and
 // loads again those that still hold the sentinel: the data is its own ready
 // flag, so no counter or fence sits between a shrink and the expands that use
 // it.  A workgroup only waits for workgroups earlier in the grid, which do not
 // wait, so every wait ends; the number of rounds is bounded all the same (past
-// it the wait gives up and sets the status flag).  The last of a row block's
-// expand items to finish arms the row block's partial blocks again.  The
-// blocks are added in the same fixed order as in the two-launch form, so both
+// it the wait gives up and sets the status flag).  The in the same fixed order as in the two-launch form, so both
 // give bit-identical results whatever the timing.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
@@ -317,21 +316,17 @@ __device__ __forceinline__ float part_sum(const float* src, int64_t pstride, int
     return s;
 }
 
-// Step launch, end of an expand item: the last of the row block's expand
-// items to finish (its departure count dep + 1 == nexp) arms the row block's
-// partial blocks again and clears its counter, for the next launch.  flag is
-// LDS that no thread reads any more.
-__device__ __forceinline__ void rearm_row_block(const KernelArgs& a, const Item& it, uint32_t dep,
-                                                int* flag) {
-    if (threadIdx.x == 0) *flag = dep + 1 == (uint32_t)it.nexp;
-    __syncthreads();
-    if (*flag) {
-        uint32_t* p = (uint32_t*)(a.partials + it.part);
-        const int n = it.nsplit * it.pstride;
-        for (int i = threadIdx.x; i < n; i += kThreads)
-            __hip_atomic_store(p + i, kSentinel, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (threadIdx.x == 0) __hip_atomic_store(a.sync + it.rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+// Step launch: the row block's two partial buffers.  Launches alternate
+// between them, the parity coming from the row block's counter of finished
+// expand items (it wraps at 2 nexp): below nexp -> buffer 0, else buffer 1.
+// Within one launch every reader sees the same parity: all shrink items of a
+// row block start before any of its expand items can finish, and an expand
+// item that reads late sees fewer than nexp increments of its own launch.
+// Each shrink item arms (sets to the sentinel) its block in the buffer the
+// next launch will use, which no item of this launch reads.
+__device__ __forceinline__ uint32_t row_block_parity(const KernelArgs& a, const Item& it) {
+    const uint32_t c = __hip_atomic_load(a.sync + (int64_t)it.rb * kSyncStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return c >= (uint32_t)it.nexp ? 1u : 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -367,6 +362,8 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     const int kv = sub / 8;
     const int nx = nrows * kv;
     const int npass = (it.len + sub - 1) / sub;
+    uint32_t parity = 0;                       // step launch: which partial buffer (read early, used last)
+    if constexpr (kSync) parity = row_block_parity(a, it);
 
     // the padding ranks of A^T stay zero for every pass
     for (int i = t; i < (Rp - R) * KP; i += kThreads) As[R * KP + i] = 0u;
@@ -499,6 +496,7 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
 
     // lane holds v[row m*16+lr][ranks tile*16 + 4lg .. +3]
     float* part = a.partials + it.part;
+    if constexpr (kSync) part += parity ? a.pbuf : 0;
     if (WK == 1) {
 #pragma unroll
         for (int m = 0; m < MS; ++m) {
@@ -540,6 +538,16 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
             for (int k = 1; k < WK; ++k) s += red[(k * MS * 16 + row) * Rp + rank];
             put_f32<kSync>(part + o, s);
         }
+    }
+    if constexpr (kSync) {
+        // arm this block in the other buffer for the next launch, after this
+        // launch's block is out.  Plain stores: only the next launch reads
+        // them, and a kernel's end makes its stores visible to the next.  The
+        // block is reserved to a multiple of 4 floats, so whole 16-byte
+        // stores stay inside it.
+        u32x4* other = (u32x4*)(a.partials + (parity ? 0 : a.pbuf) + it.part);
+        const u32x4 s4 = {kSentinel, kSentinel, kSentinel, kSentinel};
+        for (int o = t; 4 * o < nrows * R; o += kThreads) other[o] = s4;
     }
 }
 
@@ -644,6 +652,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     const int nslot = MS * 16 * half;
     const int P = a.v ? 1 : partial_parts(nrows, R, it.nsplit);
     const float* Pb = a.partials + it.part;
+    if constexpr (kSync) Pb += row_block_parity(a, it) ? a.pbuf : 0;
     int budget = a.spin_limit;                // step launch: polling rounds left to this thread
     auto sum_parts = [&]() {
         if (P > 1) {
@@ -720,9 +729,12 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         Vl[row * RP + jp] = l0 | (l1 << 16);
     }
     __syncthreads();
-    uint32_t dep = 0;   // step launch: this item's place among the row block's departures
+    // step launch: this item has read its partial values; count it (no wait
+    // for the result)
     if constexpr (kSync)
-        if (t == 0) dep = __hip_atomic_fetch_add(a.sync + it.rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (t == 0)
+            (void)__builtin_amdgcn_atomic_inc32(a.sync + (int64_t)it.rb * kSyncStride, 2u * (uint32_t)it.nexp - 1u, __ATOMIC_RELAXED,
+                                                "agent");
 
     // --- y^T = B^T v^T on MFMA, then y + s*d rounded once
     f32x4 acc[Q][MS];
@@ -766,7 +778,6 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             }
         }
     }
-    if constexpr (kSync) rearm_row_block(a, it, dep, (int*)red);
 }
 
 template <class Fmt, bool kSync>
