@@ -215,6 +215,12 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
             base.pstride = pstride;
             if (nb <= kInlineRows)
                 for (int i = 0; i < nb; ++i) base.rows[i] = p.perm[p0 + i];
+            base.row0 = p.perm[p0];
+            for (int i = 1; i < nb; ++i)
+                if (p.perm[p0 + i] != p.perm[p0] + i) {
+                    base.row0 = -1;
+                    break;
+                }
             const int64_t part0 = p.n_partials;
             p.n_partials += (int64_t)nsplit * pstride;
             for (int c = 0; c < nsplit; ++c) {

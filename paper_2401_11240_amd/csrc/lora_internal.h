@@ -86,7 +86,7 @@ struct DevItem {
     int32_t pstride;     // floats between consecutive partial blocks of the row block
     int32_t rb;          // row block index (its counter of finished expand items in the step launch)
     int32_t nexp;        // expand items of the row block
-    int32_t pad;
+    int32_t row0;        // the first row when the item's rows are consecutive (a prompt segment), else -1
     int32_t rows[kInlineRows];   // the item's rows when nrows <= kInlineRows
 };
 static_assert(sizeof(DevItem) == 128, "DevItem layout");

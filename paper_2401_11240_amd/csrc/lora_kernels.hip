@@ -102,7 +102,7 @@ struct FmtBF16 {
 // never copied as one aggregate, which would send it to scratch memory).
 struct Item {
     int64_t part;
-    int kind, group, adapter, rank, nrows, lo, len, sub, nsplit, p0, pstride, rb, nexp;
+    int kind, group, adapter, rank, nrows, lo, len, sub, nsplit, p0, pstride, rb, nexp, row0;
     int rows[kInlineRows];
     const void* fac;     // the factor this item streams: A_g (shrink) or B_g (expand)
     float scale;         // s_g
@@ -111,7 +111,7 @@ struct Item {
 // The item's two 64-byte halves are requested together (two scalar loads in
 // flight), so its inline rows cost no second round trip.
 typedef unsigned int u32x16 __attribute__((ext_vector_type(16)));
-static_assert(offsetof(DevItem, rows) == 64 && offsetof(DevItem, nexp) == 56, "DevItem halves");
+static_assert(offsetof(DevItem, rows) == 64 && offsetof(DevItem, row0) == 60, "DevItem halves");
 __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     const u32x16 w0 = ((const u32x16*)p)[0];
     const u32x16 w1 = ((const u32x16*)p)[1];
@@ -130,6 +130,7 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     it.pstride = (int)w0[12];
     it.rb = (int)w0[13];
     it.nexp = (int)w0[14];
+    it.row0 = (int)w0[15];
 #pragma unroll
     for (int q = 0; q < kInlineRows; ++q) it.rows[q] = (int)w1[q];
     return it;
@@ -212,11 +213,13 @@ __device__ __forceinline__ int write_rows(int v, const Item& it) {
 }
 
 // Lane l of every wave holds the item's row l (nrows <= 64): built from the
-// inline rows with lane writes, or read from the grouped row order.  Must be
-// called with every lane active.
+// inline rows with lane writes, counted from the first row when the rows are
+// consecutive, or read from the grouped row order.  Must be called with
+// every lane active.
 __device__ __forceinline__ int lane_rows(const KernelArgs& a, const Item& it) {
     if (it.nrows <= kInlineRows) return write_rows<0>(0, it);
     const int lane = threadIdx.x & 63;
+    if (it.row0 >= 0) return it.row0 + (lane < it.nrows ? lane : 0);
     return lane < it.nrows ? a.perm[it.p0 + lane] : 0;
 }
 // The item's r-th row, fetched from lane r (every lane active).
@@ -802,7 +805,8 @@ __device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it,
 }
 
 template <class Fmt>
-__global__ void __launch_bounds__(kThreads) lora_expand_kernel(KernelArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+lora_expand_kernel(KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLds];
     const Item it = load_item(a.items + blockIdx.x);
     if (it.kind != kItemExpand) return;
