@@ -67,6 +67,9 @@ def parse():
     ap.add_argument("--workload", default="decode_mixed")
     ap.add_argument("--prefill-workload", default="prefill")
     ap.add_argument("--prefill-steps", type=int, default=40)
+    ap.add_argument("--extra", default="llama13b_layer,llama70b_mixed",
+                    help="further named workloads timed the same way (comma-separated; empty for none)")
+    ap.add_argument("--extra-steps", type=int, default=40)
     ap.add_argument("--rotate-mib", type=float, default=640.0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -320,6 +323,26 @@ def main():
             "algorithmic_bytes_per_step": pre["bytes_per_step"],
             "rotated_copies": pre["R"],
         }
+    extras = [e for e in args.extra.split(",") if e]
+    if extras:
+        out["more"] = {}
+    for name in extras:
+        wx = W.NAMED[name]()
+        mx = measure(torch, wx, dev, args.extra_steps, max(4, args.extra_steps // 10),
+                     args.rotate_mib, name)
+        out["more"][wx.name] = {
+            "ms_per_step": mx["ms_per_step"],
+            "GBps": round(mx["gbps"], 2),
+            "pct_hbm_peak": round(100.0 * mx["gbps"] / HBM_PEAK_GBPS, 2),
+            "tokens_per_step": mx["n_active"],
+            "tokens_per_s": round(mx["tokens_per_s"], 1),
+            "TFLOPs": round(mx["flops_per_step"] / (mx["ms_per_step"] * 1e-3) / 1e12, 3),
+            "launches_per_step": mx["n_proj"],
+            "distinct_adapters": mx["distinct"],
+            "algorithmic_bytes_per_step": mx["bytes_per_step"],
+            "rotated_copies": mx["R"],
+        }
+        del wx
     if args.calibrate_copy_mib > 0:
         n = int(args.calibrate_copy_mib * 2 ** 20)
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)

@@ -95,9 +95,10 @@ struct HostPlan {
     int r_max = 0;
     int n_rb = 0;                       // row blocks
     std::vector<int32_t> perm, group_off, group_adapter, group_rank;
-    std::vector<DevItem> shrink, expand, reduce;
+    std::vector<DevItem> shrink, expand, reduce, reduce_all;
+    int n_rows = 0;
     int64_t n_partials = 0;
-    size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_perm = 0;
+    size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_reduce_all = 0, off_perm = 0;
     size_t plan_bytes = 0, off_partials = 0, off_sync = 0, sync_bytes = 0, total_bytes = 0;
     size_t off_step_partials = 0, step_partials_bytes = 0, plan_total_bytes = 0;
     std::vector<unsigned char> blob;
@@ -169,6 +170,8 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.shrink.clear();
     p.expand.clear();
     p.reduce.clear();
+    p.reduce_all.clear();
+    p.n_rows = b->n_rows;
     p.n_partials = 0;
     p.n_rb = 0;
 
@@ -188,6 +191,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     for (int g = 0; g < p.n_groups; ++g) {
         const DevAdapter& ad = t->host[p.group_adapter[g]];
         const int r = ad.rank;
+        const int rv = rank_stride(r);
         p.group_rank[g] = r;
         p.r_max = std::max(p.r_max, r);
         const int rb = row_block(r);
@@ -200,7 +204,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
                 krange = round_up_i(std::max(per, sub), sub);
             }
             const int nsplit = (t->h_in + krange - 1) / krange;
-            const int pstride = round_up_i(nb * r, 4);
+            const int pstride = nb * rv;              // one partial (or v) block: [nb][rv] floats
             const int nlen = expand_nlen(r, nb);
             const int ntiles = (t->h_out + nlen - 1) / nlen;
             DevItem base{};
@@ -221,8 +225,11 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
                     base.row0 = -1;
                     break;
                 }
+            // the row block's nsplit partial blocks, then its v block
             const int64_t part0 = p.n_partials;
-            p.n_partials += (int64_t)nsplit * pstride;
+            p.n_partials += (int64_t)(nsplit + 1) * pstride;
+            // small partial blocks are added up by the expand items themselves
+            const bool direct = nsplit <= kDirectSplits && (int64_t)nsplit * pstride * 4 <= kDirectBytes;
             for (int c = 0; c < nsplit; ++c) {
                 DevItem it = base;
                 it.kind = kItemShrink;
@@ -234,36 +241,65 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
                     return fail(LORA_E_SHAPE, "internal: shrink tile exceeds LDS");
                 p.shrink.push_back(it);
             }
+            // reduce slices: at most kReduceBytes of partial values each; G
+            // split groups share a float4 position (G * positions <= threads),
+            // each thread adding at most kMaxSplitLoads blocks
+            int gmin = 1;
+            while (gmin * kMaxSplitLoads < nsplit) gmin *= 2;
+            const int64_t pbytes = (int64_t)nsplit * pstride * 4;
+            int nslice = (int)std::max<int64_t>(1, (pbytes + kReduceBytes - 1) / kReduceBytes);
+            int slen = round_up_i((pstride + nslice - 1) / nslice, 4);
+            slen = std::min(slen, 4 * (kThreads / gmin));
+            nslice = (pstride + slen - 1) / slen;
+            for (int c = 0; c < nslice; ++c) {
+                DevItem it = base;
+                it.kind = kItemReduce;
+                it.part = part0;
+                it.lo = c * slen;
+                it.len = std::min(slen, pstride - c * slen);
+                const int np = it.len / 4;
+                int G = 1;
+                // a row block whose expand items add the partial blocks up
+                // themselves adds them in order 0..nsplit-1: one group here too
+                while (!direct && 2 * G <= nsplit && 2 * G * np <= kThreads) G *= 2;
+                if (G * kMaxSplitLoads < nsplit) return fail(LORA_E_SHAPE, "internal: reduce slice too wide");
+                it.sub = G;
+                p.reduce_all.push_back(it);         // lora_shrink's reduce into the caller's v
+                if (!direct) p.reduce.push_back(it);
+            }
             for (int c = 0; c < ntiles; ++c) {
                 DevItem it = base;
                 it.kind = kItemExpand;
                 it.part = part0;
+                it.sub = direct ? 1 : 0;
                 it.lo = c * nlen;
                 it.len = std::min(nlen, t->h_out - c * nlen);
-                if (expand_lds_bytes(r, it.len, nb) > kExpandLds)
+                if (expand_lds_bytes(r, nb) > kExpandLds)
                     return fail(LORA_E_SHAPE, "internal: expand tile exceeds LDS");
                 p.expand.push_back(it);
             }
-            DevItem it = base;
-            it.kind = kItemReduce;
-            it.part = part0;
-            p.reduce.push_back(it);
         }
     }
 
-    // device layout: [shrink items][expand items][reduce items][perm] |
-    // [partials][row block counters, status] (a workspace ends here) |
-    // [step partials x 2] (plans only: the step launch's partial blocks in two
-    // buffers used by alternate launches, each armed with the sentinel before
-    // the launch that reads it).  The expand items follow the shrink
-    // items directly: the step launch runs both lists as one grid.
+    if ((uint64_t)p.n_partials * 4 > kMaxSpan)
+        return fail(LORA_E_SHAPE, "batch too large: its partial results exceed 2 GiB");
+
+    // device layout: [shrink items][reduce items][expand items][all reduce
+    // items][perm] |
+    // [partial and v blocks][row block counters, status] (a workspace ends
+    // here) | [step partial and v blocks x 2] (plans only: the step launch's
+    // blocks in two buffers used by alternate launches, each armed with the
+    // sentinel before the launch that reads it).  The three item lists are
+    // contiguous: the step launch runs them as one grid.
     size_t off = 0;
     p.off_shrink = off;
     off += p.shrink.size() * sizeof(DevItem);
-    p.off_expand = off;
-    off = align_up(off + p.expand.size() * sizeof(DevItem));
     p.off_reduce = off;
-    off = align_up(off + p.reduce.size() * sizeof(DevItem));
+    off += p.reduce.size() * sizeof(DevItem);
+    p.off_expand = off;
+    off += p.expand.size() * sizeof(DevItem);
+    p.off_reduce_all = off;
+    off = align_up(off + p.reduce_all.size() * sizeof(DevItem));
     p.off_perm = off;
     off = align_up(off + p.perm.size() * sizeof(int32_t));
     p.plan_bytes = off;
@@ -282,8 +318,9 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
         if (n) std::memcpy(p.blob.data() + at, src, n);
     };
     put(p.off_shrink, p.shrink.data(), p.shrink.size() * sizeof(DevItem));
-    put(p.off_expand, p.expand.data(), p.expand.size() * sizeof(DevItem));
     put(p.off_reduce, p.reduce.data(), p.reduce.size() * sizeof(DevItem));
+    put(p.off_expand, p.expand.data(), p.expand.size() * sizeof(DevItem));
+    put(p.off_reduce_all, p.reduce_all.data(), p.reduce_all.size() * sizeof(DevItem));
     put(p.off_perm, p.perm.data(), p.perm.size() * sizeof(int32_t));
     return LORA_OK;
 }
@@ -402,16 +439,26 @@ int check_ws(const HostPlan& p, const void* ws, size_t ws_bytes) {
     return LORA_OK;
 }
 
-int check_x(const lora_table_s* t, const void* x, int64_t ldx) {
-    if (!x) return fail(LORA_E_ARG, "x is NULL");
-    if (!aligned16(x)) return fail(LORA_E_ALIGN, "x not 16-byte aligned");
-    return check_ld("ldx", ldx, t->h_in);
+// Bytes from the first element of a [n_rows, ld] matrix to the end of its
+// last row of h elements.
+uint64_t span_bytes(int n_rows, int64_t ld, int h) {
+    return n_rows > 0 ? ((uint64_t)(n_rows - 1) * (uint64_t)ld + (uint64_t)h) * 2 : 0;
 }
 
-int check_y(const lora_table_s* t, const void* y, int64_t ldy) {
+int check_x(const lora_table_s* t, const void* x, int64_t ldx, int n_rows) {
+    if (!x) return fail(LORA_E_ARG, "x is NULL");
+    if (!aligned16(x)) return fail(LORA_E_ALIGN, "x not 16-byte aligned");
+    if (int rc = check_ld("ldx", ldx, t->h_in)) return rc;
+    if (span_bytes(n_rows, ldx, t->h_in) > kMaxSpan) return fail(LORA_E_SHAPE, "x spans more than 2 GiB");
+    return LORA_OK;
+}
+
+int check_y(const lora_table_s* t, const void* y, int64_t ldy, int n_rows) {
     if (!y) return fail(LORA_E_ARG, "y is NULL");
     if (!aligned16(y)) return fail(LORA_E_ALIGN, "y not 16-byte aligned");
-    return check_ld("ldy", ldy, t->h_out);
+    if (int rc = check_ld("ldy", ldy, t->h_out)) return rc;
+    if (span_bytes(n_rows, ldy, t->h_out) > kMaxSpan) return fail(LORA_E_SHAPE, "y spans more than 2 GiB");
+    return LORA_OK;
 }
 
 int check_v(const HostPlan& p, const void* v, int64_t ldv) {
@@ -423,16 +470,23 @@ int check_v(const HostPlan& p, const void* v, int64_t ldv) {
 }
 
 // Enqueue the shrink (x != NULL) and/or the expand (y != NULL) of plan p on
-// table t with its workspace at w, as two launches.
+// table t with its workspace at w, as separate launches: shrink, then (unless
+// the caller reduces into its own v) reduce into the v blocks; expand.
 int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x, int64_t ldx,
-            void* y, int64_t ldy, hipStream_t s) {
+            void* y, int64_t ldy, hipStream_t s, bool v_out = false) {
     if (x) {
         KernelArgs a = make_args(t, p, w, kSpinLimit);
         a.items = (const DevItem*)(w + p.off_shrink);
         a.n_items = (int32_t)p.shrink.size();
         a.x = x;
         a.ldx = ldx;
+        a.x_bytes = (uint32_t)span_bytes(p.n_rows, ldx, t->h_in);
         LORA_HIP_TRY(launch_shrink(a, t->dtype, s));
+        if (!v_out) {
+            a.items = (const DevItem*)(w + p.off_reduce);
+            a.n_items = (int32_t)p.reduce.size();
+            LORA_HIP_TRY(launch_reduce(a, s));
+        }
     }
     if (y) {
         KernelArgs a = make_args(t, p, w, kSpinLimit);
@@ -440,6 +494,7 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
         a.n_items = (int32_t)p.expand.size();
         a.y = y;
         a.ldy = ldy;
+        a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
         LORA_HIP_TRY(launch_expand(a, t->dtype, s));
     }
     return LORA_OK;
@@ -453,11 +508,13 @@ int enqueue_step(const lora_table_s* t, const HostPlan& p, unsigned char* w, con
     KernelArgs a = make_args(t, p, w, spin_limit);
     a.partials = (float*)(w + p.off_step_partials);
     a.items = (const DevItem*)(w + p.off_shrink);
-    a.n_items = (int32_t)(p.shrink.size() + p.expand.size());
+    a.n_items = (int32_t)(p.shrink.size() + p.reduce.size() + p.expand.size());
     a.x = x;
     a.ldx = ldx;
+    a.x_bytes = (uint32_t)span_bytes(p.n_rows, ldx, t->h_in);
     a.y = y;
     a.ldy = ldy;
+    a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
     LORA_HIP_TRY(launch_step(a, t->dtype, s));
     return LORA_OK;
 }
@@ -504,6 +561,8 @@ int lora_register_adapters(lora_table_t* out, int device, int h_in, int h_out, i
     if (n_adapters < 0) return fail(LORA_E_ARG, "negative n_adapters");
     if (h_in <= 0 || h_out <= 0 || h_in % 8 || h_out % 8)
         return fail(LORA_E_SHAPE, "h_in and h_out must be positive multiples of 8");
+    if ((uint64_t)std::max(h_in, h_out) * kMaxRank * 2 > kMaxSpan)
+        return fail(LORA_E_SHAPE, "h_in and h_out must be at most 4 Mi elements (factors below 2 GiB)");
     if (n_adapters > 0 && (!A_ptrs || !B_ptrs || !ranks || !scales))
         return fail(LORA_E_ARG, "adapter arrays must not be NULL");
     std::vector<DevAdapter> host(n_adapters);
@@ -590,17 +649,17 @@ int lora_shrink(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ld
     HostPlan p;
     if (int rc = build_plan(t, b, p)) return rc;
     if (p.n_active == 0) return LORA_OK;
-    if (int rc = check_x(t, x, ldx)) return rc;
+    if (int rc = check_x(t, x, ldx, b->n_rows)) return rc;
     if (int rc = check_v(p, v, ldv)) return rc;
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
-    if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s)) return rc;
+    if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s, true)) return rc;
     KernelArgs a = make_args(t, p, w, kSpinLimit);
-    a.items = (const DevItem*)(w + p.off_reduce);
-    a.n_items = (int32_t)p.reduce.size();
+    a.items = (const DevItem*)(w + p.off_reduce_all);
+    a.n_items = (int32_t)p.reduce_all.size();
     a.v = v;
     a.ldv = ldv;
     LORA_HIP_TRY(launch_reduce(a, s));
@@ -614,7 +673,7 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
     if (int rc = build_plan(t, b, p)) return rc;
     if (p.n_active == 0) return LORA_OK;
     if (int rc = check_v(p, v, ldv)) return rc;
-    if (int rc = check_y(t, y, ldy)) return rc;
+    if (int rc = check_y(t, y, ldy, b->n_rows)) return rc;
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
@@ -627,6 +686,7 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
     a.ldv = ldv;
     a.y = y;
     a.ldy = ldy;
+    a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
     LORA_HIP_TRY(launch_expand(a, t->dtype, s));
     return LORA_OK;
 }
@@ -637,8 +697,8 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
     HostPlan p;
     if (int rc = build_plan(t, b, p)) return rc;
     if (p.n_active == 0) return LORA_OK;
-    if (int rc = check_x(t, x, ldx)) return rc;
-    if (int rc = check_y(t, y, ldy)) return rc;
+    if (int rc = check_x(t, x, ldx, b->n_rows)) return rc;
+    if (int rc = check_y(t, y, ldy, b->n_rows)) return rc;
     if (int rc = check_overlap(x, ldx, t->h_in, y, ldy, t->h_out, b->n_rows)) return rc;
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
@@ -686,9 +746,9 @@ static int plan_run(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, 
     if (int rc = check_compatible(pl->plan, tt)) return rc;
     if (pl->plan.n_active == 0) return LORA_OK;
     if (x)
-        if (int rc = check_x(tt, x, ldx)) return rc;
+        if (int rc = check_x(tt, x, ldx, pl->n_rows)) return rc;
     if (y)
-        if (int rc = check_y(tt, y, ldy)) return rc;
+        if (int rc = check_y(tt, y, ldy, pl->n_rows)) return rc;
     if (x && y)
         if (int rc = check_overlap(x, ldx, tt->h_in, y, ldy, tt->h_out, pl->n_rows)) return rc;
     DeviceGuard dg(tt->device);

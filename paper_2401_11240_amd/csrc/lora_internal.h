@@ -3,34 +3,42 @@
 // A step is planned on the host into flat lists of work items, one per
 // workgroup.  Rows are first grouped by adapter (the per-token gather of
 // Sections 2.3 C2 / 4.1) and each group is cut into row blocks of at most
-// 64 rows.  Every row block's adapter is cut into pieces of about 32 KiB:
-// shrink items stream a K range of A_g (rows k0..k0+len of the [h_in, r]
-// matrix), expand items one column tile of B_g.  The piece's extent in rows or
-// columns shrinks as the rank grows, so every item moves about the same number
-// of bytes whatever its rank (padding-free: the cost follows the sum of ranks,
-// Section 5), and items of every rank run side by side in one grid.
+// 64 rows.  Each row block then becomes three kinds of items:
 //
-// The shrink writes one float32 partial block per (row block, K range); the
-// expand adds a row block's partial blocks in a fixed order while it stages v,
-// so results never depend on timing.  The two run either as two launches (the
-// launch boundary orders them) or as one step launch whose grid holds every
-// shrink item before every expand item: a shrink workgroup writes its block
-// with device-coherent stores into a buffer armed with a sentinel pattern
-// (two buffers, used by alternate launches); an expand workgroup requests its
-// B tile and its y values, then loads the partial values, again while any
-// still holds the sentinel.  It only ever
-// waits for workgroups earlier in the grid, which never wait themselves, and
-// the wait is bounded (it gives up and raises a status flag).
+//   shrink  (row block, K range of A_g): a float32 partial block
+//           P_c[row, 0:Rv] = sum over the K range of x[row, k] A_g[k, :];
+//   reduce  (row block, slice of its v block): v = sum_c P_c over that slice,
+//           the partial blocks added in a fixed order;
+//   expand  (row block, column tile of B_g): y[row, tile] is rounded once
+//           from y + s_g * v[row, :] . B_g[:, tile].
+//
+// A K range streams about the same number of bytes whatever the rank
+// (padding-free: the cost follows the sum of ranks, Section 5), and items of
+// every rank run side by side in one grid.  The reduce items cut the row
+// block's v into slices so that no item adds up more than a few tens of KB of
+// partial values, and every expand tile reads the finished v once (a few KB)
+// instead of the partial blocks.
+//
+// The three kinds run either as separate launches (launch boundaries order
+// them) or as one step launch whose grid holds every shrink item, then every
+// reduce item, then every expand item.  In the step launch the partial and v
+// blocks live in two buffers used by alternate launches and hold a sentinel
+// pattern until written; a consumer loads the values it needs with
+// device-coherent loads and loads again those that still hold the sentinel.
+// Every wait is on items earlier in the grid, which never wait on later ones,
+// and the wait is bounded (it gives up and raises a status flag).
 //
 // A plan depends on the batch, the ranks and the shapes only.  The weight
 // pointers and scales of the groups it references travel in the kernel
 // arguments of each launch, so one plan serves every layer's adapter table of
 // the same ranks (the batch of a step is the same for all of them).
 //
-// Both kernels run the contraction on MFMA: the shrink as v^T = A^T x^T
-// (16x16x32, K = h_in), the expand as y^T = B^T v^T (16x16x16, K = rank).  The
-// factor tile is staged in LDS transposed into words holding two consecutive
-// K elements, so every MFMA operand fragment is one LDS vector read.
+// Both contractions run on MFMA (v_mfma_f32_16x16x32).  Shrink: v^T = A^T x^T,
+// K = h_in; A is transposed in registers (8 K rows x 8 ranks per lane) and
+// staged in LDS as 16-byte chunks of 8 consecutive K of one rank.  Expand:
+// y^T = B^T v^T with the 32 K slots holding 16 ranks twice, once with the
+// high and once with the low 16-bit part of v (v is never rounded to a single
+// 16-bit value); B is transposed in registers, no LDS.
 #pragma once
 #include <stdint.h>
 
@@ -47,17 +55,24 @@ constexpr int kMaxRank = 256;
 constexpr int kMSub = 4;                 // 16-row MFMA subtiles per item at most
 constexpr int kInlineRows = 16;          // items this small carry their rows inline
 constexpr int kKargGroups = 128;         // groups whose pointers travel in the kernel arguments
-constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink kernel
-constexpr int kExpandLds = 68 * 1024;    // LDS bytes of the expand kernel
-constexpr int kStepLds = kExpandLds > kShrinkLds ? kExpandLds : kShrinkLds;
+constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink body
+constexpr int kExpandLds = 32 * 1024;    // LDS bytes of the expand body (v fragments)
+constexpr int kReduceLds = kThreads * 16;
+constexpr int kStepLds = kShrinkLds;
 constexpr int kSyncStride = 32;          // 32-bit words between row block counters (one 128-byte line each)
+constexpr int kReduceBytes = 32 * 1024;  // partial bytes one reduce item adds up at most
+constexpr int kDirectBytes = 16 * 1024;  // partial bytes up to which expand items add them up themselves
+constexpr int kMaxSplitLoads = 16;       // partial blocks one reduce thread adds up
+constexpr int kDirectSplits = 8;         // partial blocks an expand item adds up itself, at most
+constexpr uint32_t kMaxSpan = 0x7fff0000u;  // x, y, factor and partial spans stay below 2 GiB (buffer offsets)
+static_assert(kExpandLds <= kStepLds && kReduceLds <= kStepLds, "step LDS");
 
 // Item kinds.
 enum : int32_t {
     kItemNop = 0,
     kItemShrink = 1,     // part = x(rows, k0:k0+len) . A(k0:k0+len, 0:r)
-    kItemExpand = 2,     // y(rows, n0:n0+len) += s * (sum of parts) . B(0:r, n0:n0+len)
-    kItemReduce = 3,     // v(rows, 0:r) = sum of parts
+    kItemExpand = 2,     // y(rows, n0:n0+len) += s * v . B(0:r, n0:n0+len)
+    kItemReduce = 3,     // v slice = sum of the row block's partial blocks
 };
 
 // One registered adapter, as the device-resident registry holds it (32 B).
@@ -71,19 +86,27 @@ struct DevAdapter {
 static_assert(sizeof(DevAdapter) == 32, "DevAdapter layout");
 
 // One work item = one workgroup (128 bytes, read with scalar loads).
+//   shrink: part = its partial block; lo, len = K range; sub = K per pass
+//   reduce: part = first partial block of the row block (the v block follows
+//           the nsplit partial blocks); lo = first float of the slice, len =
+//           its floats (multiple of 4); sub = split groups (see reduce_body)
+//   expand: part = first partial block of the row block (the v block follows
+//           the nsplit partial blocks); lo, len = column tile; sub = 1 when
+//           the item adds up the partial blocks itself (no reduce items for
+//           a row block whose partial blocks are small), else 0
 struct DevItem {
-    int64_t part;        // float offset: shrink -> its own partial block; expand/reduce -> the row block's first
+    int64_t part;        // float offset into the partial buffer
     int32_t kind;
     int32_t group;       // group of the batch (index into the launch's pointer table)
     int32_t adapter;     // adapter index (registry fallback when group >= kKargGroups)
     int32_t rank;
     int32_t nrows;       // rows in this item (<= 64)
-    int32_t lo;          // k0 (shrink) or n0 (expand)
-    int32_t len;         // K range (shrink) or column tile (expand), multiple of 8
-    int32_t sub;         // shrink: K sub-chunk staged per pass (multiple of 32)
-    int32_t nsplit;      // expand / reduce: partial blocks to add
+    int32_t lo;
+    int32_t len;
+    int32_t sub;
+    int32_t nsplit;      // partial blocks of the row block
     int32_t p0;          // position of the first row in the grouped row order (perm)
-    int32_t pstride;     // floats between consecutive partial blocks of the row block
+    int32_t pstride;     // floats of one partial block (= nrows * rv)
     int32_t rb;          // row block index (its counter of finished expand items in the step launch)
     int32_t nexp;        // expand items of the row block
     int32_t row0;        // the first row when the item's rows are consecutive (a prompt segment), else -1
@@ -95,7 +118,7 @@ struct KernelArgs {
     const DevItem* items;
     const int32_t* perm;        // grouped row order
     const DevAdapter* table;    // registry (fallback for groups beyond the argument table)
-    float* partials;            // split-K partial blocks
+    float* partials;            // partial and v blocks
     const void* x;
     int64_t ldx;
     void* y;
@@ -110,6 +133,8 @@ struct KernelArgs {
     int32_t* status;            // step launch: set to 1 when a wait gave up
     int64_t pbuf;               // step launch: floats from the first partial buffer to the second
     int32_t spin_limit;         // step launch: polling rounds before a wait gives up
+    uint32_t x_bytes;           // bytes from x to the end of its last row (< 2 GiB)
+    uint32_t y_bytes;           // bytes from y to the end of its last row (< 2 GiB)
     int32_t pad;
     const void* gfac[2 * kKargGroups];   // per group g: [2g] = A_g, [2g + 1] = B_g
     float gscale[kKargGroups];           // per group: s_g
@@ -117,68 +142,80 @@ struct KernelArgs {
 static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 
 // ---------------------------------------------------------------------------
-// Tiling, shared by the planner (sizes the items) and the kernels (lays out
+// Tiling, shared by the planner (sizes the items) and the kernels (lay out
 // LDS).  All extents are in elements unless named *_bytes.
 // ---------------------------------------------------------------------------
 LORA_HD inline int round_up_i(int v, int m) { return (v + m - 1) / m * m; }
 LORA_HD inline int min_i(int a, int b) { return a < b ? a : b; }
 LORA_HD inline int max_i(int a, int b) { return a > b ? a : b; }
 LORA_HD inline int msub_of(int nrows) { return (nrows + 15) / 16; }
-// MFMA subtiles the kernel body is compiled for: 1, 2 or 4
+// MFMA subtiles the kernel bodies are compiled for: 1, 2 or 4
 LORA_HD inline int msub_body(int nrows) { const int m = msub_of(nrows); return m <= 1 ? 1 : (m <= 2 ? 2 : 4); }
 
-// Rows per row block: 64, or 32 when the rank pads past 128 (expand LDS).
+// Row stride of partial and v blocks: the rank rounded up to 8 floats.
+LORA_HD inline int rank_stride(int rank) { return round_up_i(rank, 8); }
+
+// Rows per row block: 64, or 32 when the rank pads past 128.
 LORA_HD inline int row_block(int rank) { return round_up_i(rank, 16) > 128 ? 32 : 64; }
 
-// Shrink: ranks padded to 16 (MFMA N); the K sub-chunk staged per pass is a
-// multiple of 32 (MFMA K) with an A^T tile of at most 32 KiB.
-LORA_HD inline int shrink_sub(int rank, int nrows) {
-    const int rp = round_up_i(rank, 16);
-    const int k = min_i(16384 / rp, 512 / msub_body(nrows)) & ~31;
-    return max_i(32, k);
-}
-LORA_HD inline int shrink_kp(int sub) { return sub / 2 + 4; }   // words per A^T row, 4 (mod 8)
-LORA_HD inline int shrink_kx(int sub) { return sub + 8; }       // halves per x row
-LORA_HD inline int shrink_wn(int rank) {
+// ---- shrink ----
+// A pass stages `sub` K (a multiple of 32) of A^T and of the row block's x
+// in LDS, each row as sub/8 + 1 chunks of 16 bytes (an odd chunk stride: 16-
+// byte reads and writes of eight consecutive lanes hit distinct banks).
+LORA_HD inline int shrink_chunks(int sub) { return sub / 8 + 1; }
+LORA_HD inline int shrink_wn(int rank) {     // waves side by side over rank tiles: 1, 2 or 4
     const int nt = round_up_i(rank, 16) / 16;
     return nt >= 4 ? 4 : (nt >= 2 ? 2 : 1);
 }
-LORA_HD inline int shrink_tq(int rank) {    // rank tiles per wave: 1, 2 or 4
+LORA_HD inline int shrink_tq(int rank) {     // rank tiles per wave: 1, 2 or 4
     const int nt = round_up_i(rank, 16) / 16;
     const int q = (nt + shrink_wn(rank) - 1) / shrink_wn(rank);
     return q <= 1 ? 1 : (q <= 2 ? 2 : 4);
 }
 LORA_HD inline int shrink_lds_bytes(int rank, int sub, int nrows) {
     const int rp = round_up_i(rank, 16);
-    const int staged = rp * shrink_kp(sub) * 4 + msub_body(nrows) * 16 * shrink_kx(sub) * 2;
+    const int staged = (rp + msub_body(nrows) * 16) * shrink_chunks(sub) * 16;
     const int wk = 4 / shrink_wn(rank);
-    const int red = wk > 1 ? wk * msub_body(nrows) * 16 * rp * 4 : 0;
+    const int red = wk > 1 ? wk * msub_body(nrows) * 16 * (rp + 4) * 4 : 0;   // rows padded by 4 floats
     return max_i(staged, red);
 }
-
-// Expand: ranks padded to 16 (MFMA K); a column tile of 64 * q columns, q in
-// {1, 2, 4, 8} with q * msub <= 16 (register budget) and the B^T tile within
-// LDS.
-LORA_HD inline int expand_rp(int rank) { return round_up_i(rank, 16) / 2 + 2; }  // words per row, 2 (mod 4)
-LORA_HD inline int expand_nlen(int rank, int nrows) {
-    const int cap = 8704 / expand_rp(rank);
-    int n = 512;
-    while (n > 64 && (n > cap || (n / 64) * msub_body(nrows) > 16)) n >>= 1;
-    return n;
-}
-// The partial blocks of a row block are added in P interleaved parts (part q
-// takes blocks q, q+P, ...; the parts are then added in order q = 0..P-1), P
-// fixed by the row block's shape so that every reader adds in the same order.
-LORA_HD inline int partial_parts(int nrows, int rank, int nsplit) {
-    const int slots = nrows * round_up_i(rank, 16) / 2;
-    int p = 1;
-    while (p < 16 && 2 * p * slots <= kThreads && 2 * p <= nsplit) p *= 2;
-    return p;
+// K per pass: a multiple of 32 with the A pass at most 32 KiB (sub * rank <=
+// 16384), at most 4 x chunks per thread (msub * sub <= 512), eight-row units
+// of the A transpose covering it (see shrink_body), and the staging within LDS.
+LORA_HD inline int shrink_sub(int rank, int nrows) {
+    const int ms = msub_body(nrows);
+    int k = 512 / ms;
+    if (rank % 8 == 0) {
+        const int vpr = rank / 8;
+        k = min_i(k, 64 * (32 / vpr));
+    }
+    k = min_i(k, 16384 / round_up_i(rank, 8));
+    k &= ~31;
+    while (k > 32 && shrink_lds_bytes(rank, k, nrows) > kShrinkLds) k -= 32;
+    return max_i(32, k);
 }
 
-LORA_HD inline int expand_lds_bytes(int rank, int len, int nrows) {
-    const int rp = expand_rp(rank);
-    return round_up_i(len, 16) * rp * 4 + 2 * msub_body(nrows) * 16 * rp * 4 + kThreads * 8;
+// ---- expand ----
+// Column tiles of 256 * q columns (q column blocks of 64 per wave) with
+// q * msub <= 4 (registers) and a B tile of about 32 KiB.  Ranks are taken in
+// groups of ksg steps of 16 (q * ksg = 4 or less): every B load of a group is
+// in flight at once.
+LORA_HD inline int expand_q(int rank, int nrows) {
+    const int ms = msub_body(nrows);
+    const int rk = round_up_i(rank, 16);
+    int q = 32768 / (rk * 512);
+    q = q >= 4 ? 4 : (q >= 2 ? 2 : 1);
+    while (q * ms > 4) q >>= 1;
+    return q;
+}
+LORA_HD inline int expand_ksg(int rank, int nrows) {
+    const int ks = round_up_i(rank, 16) / 16;
+    const int cap = 4 / expand_q(rank, nrows);
+    return ks >= cap ? cap : (ks >= 2 ? 2 : 1);
+}
+LORA_HD inline int expand_nlen(int rank, int nrows) { return 256 * expand_q(rank, nrows); }
+LORA_HD inline int expand_lds_bytes(int rank, int nrows) {
+    return msub_body(nrows) * (round_up_i(rank, 16) / 16) * 64 * 16;
 }
 
 }  // namespace lora

@@ -3,47 +3,57 @@
 //
 // Shrink: one workgroup per (row block of an adapter group, K range of A_g).
 // A's rows k0..k0+len are one contiguous run of bytes, read once per step
-// with 16-byte loads however many tokens use the adapter: tokens are gathered
-// to their adapter instead of each token re-reading it (Section 4.1's gather,
-// done once per distinct adapter).  The range is staged in passes: A goes to
-// LDS transposed into words that hold two consecutive K elements of one rank,
-// the row block's x columns go to LDS as they are, and the next pass's loads
-// are in flight while the current pass runs on v_mfma_f32_16x16x32
-// (v^T[r, t] = sum_k A[k, r] x[t, k], 16 ranks x 16 rows x 32 K per
-// instruction, float32 accumulation).  When a rank has fewer tiles than waves,
-// the waves split K and add their sums through LDS in wave order.  The
-// workgroup writes its float32 partial block.
+// however many tokens use the adapter: tokens are gathered to their adapter
+// instead of each token re-reading it (Section 4.1's gather, done once per
+// distinct adapter).  Each lane loads eight consecutive K rows of eight
+// ranks (16-byte loads, a wave covering whole rows), transposes the 8 x 8
+// block in registers and writes eight 16-byte chunks of A^T to LDS; x goes to
+// LDS as it is.  The pass runs on v_mfma_f32_16x16x32 (v^T[r, t] = sum_k
+// A[k, r] x[t, k], float32 accumulation) while the next pass's loads are in
+// flight.  When a rank has fewer tiles than waves, the waves split K and add
+// their sums through LDS in wave order.  The workgroup writes its float32
+// partial block.
 //
-// Expand: one workgroup per (row block, column tile of B_g).  It adds the row
-// block's partial blocks in a fixed order (v stays float32 up to here),
-// splits each v into a high and a low 16-bit part so that v is never rounded
-// to one 16-bit value, stages the B tile in LDS transposed into rank pairs and
-// runs y^T[n, t] = sum_j B[j, n] v[t, j] on v_mfma_f32_16x16x16 (two
-// instructions per step: high and low part).  Each lane then holds four
-// consecutive columns of one row of y; y + s*d is rounded once to the storage
-// dtype and written with 8-byte stores.  The B tile, the y values and the
-// partial blocks are all requested before the first barrier.
+// Reduce: one workgroup per slice of a row block's v.  Every position of the
+// slice is the sum of the row block's partial blocks in a fixed order.
+//
+// Expand: one workgroup per (row block, column tile of B_g).  v is staged in
+// LDS as MFMA operand fragments holding its high and low 16-bit parts, so v
+// is never rounded to one 16-bit value.  Each wave streams B for its column
+// blocks straight into registers: a lane loads four columns of four
+// consecutive ranks (8-byte loads, sixteen lanes covering a 128-byte row
+// segment) and transposes them into four operand fragments.  y^T = B^T v^T
+// runs on v_mfma_f32_16x16x16, one instruction for the high and one for the
+// low part of v.  Each lane then holds 16 columns of one row; y + s*d is
+// rounded once to the storage dtype and written with 16-byte stores.  The B
+// tile and the y values are requested before v is read.  A row block whose
+// partial blocks are small has no reduce items: its expand items add the
+// partial blocks up themselves.
+//
+// Masked loads and stores are buffer operations whose offset is moved out of
+// the buffer's range: they read zeros or are dropped, with no branch.
 //
 // Rank is a runtime value: any rank in [1, 256] runs the same code (padded to
 // a multiple of 16 inside LDS and registers only), so items of different
 // ranks share one grid; the bodies are compiled for the number of rank tiles
-// (or column tiles) per wave and of 16-row subtiles, so the MFMA loops have no
-// branches.
+// (or column blocks and rank steps) per wave and of 16-row subtiles, so the
+// MFMA loops have no branches.
 //
-// Step launch: one grid holds every shrink item, then every expand item.  Its
-// partial blocks live in two buffers of their own, used by alternate
-// launches; the one a launch reads holds a sentinel bit pattern until it is
-// written.  A shrink workgroup writes its block with device-coherent stores
-// (the L2 caches of the XCDs are not coherent with each other; these stores
-// write through to the common level instead of flushing a cache) and arms its
-// block in the other buffer for the next launch.  An expand workgroup requests its B tile and its y values, stages
-// B^T, then loads the partial values it needs with device-coherent loads and
-// loads again those that still hold the sentinel: the data is its own ready
-// flag, so no counter or fence sits between a shrink and the expands that use
-// it.  A workgroup only waits for workgroups earlier in the grid, which do not
-// wait, so every wait ends; the number of rounds is bounded all the same (past
-// it the wait gives up and sets the status flag).  The in the same fixed order as in the two-launch form, so both
-// give bit-identical results whatever the timing.
+// Step launch: one grid holds every shrink item, then every reduce item, then
+// every expand item.  Its partial and v blocks live in two buffers used by
+// alternate launches; the one a launch reads holds a sentinel bit pattern until
+// it is written.  Producers write with device-coherent stores (the L2 caches
+// of the XCDs are not coherent with each other; these stores write through to
+// the common level instead of flushing a cache) and arm their block in the
+// other buffer for the next launch.  A consumer requests what it can first (B
+// tile, y values), then loads the values it waits for with device-coherent
+// loads and loads again those that still hold the sentinel: the data is its
+// own ready flag, so no counter or fence sits between producer and consumer.
+// A workgroup only waits for workgroups earlier in the grid, which do not wait
+// for later ones, so every wait ends; the number of rounds is bounded all the
+// same (past it the wait gives up and sets the status flag).  The partial
+// blocks are added in the same fixed order as in the separate launches, so
+// both give bit-identical results whatever the timing.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
@@ -53,9 +63,9 @@ namespace lora {
 
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
-typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 // Native vectors (not HIP's struct vector types): selects stay in registers.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
@@ -63,6 +73,7 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 // global memory, said explicitly so that the loads are global, not flat.
 typedef __attribute__((address_space(1))) const uint16_t gu16;
 typedef __attribute__((address_space(1))) const u32x4 gu32x4;
+typedef __attribute__((address_space(1))) const u32x2 gu32x2;
 
 // ---------------------------------------------------------------------------
 // 16-bit storage formats and their MFMA instructions
@@ -133,11 +144,16 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     it.row0 = (int)w0[15];
 #pragma unroll
     for (int q = 0; q < kInlineRows; ++q) it.rows[q] = (int)w1[q];
+    it.fac = nullptr;
+    it.scale = 0.f;
     return it;
 }
 
 __device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xffffu; }
 __device__ __forceinline__ uint32_t hi16(uint32_t w) { return w >> 16; }
+// two 16-bit values (their low halves) in one word: a low, b high
+__device__ __forceinline__ uint32_t pack_lo(uint32_t a, uint32_t b) { return (a & 0xffffu) | (b << 16); }
+__device__ __forceinline__ uint32_t pack_hi(uint32_t a, uint32_t b) { return (a >> 16) | (b & 0xffff0000u); }
 
 // Where the factor pointers and scales of a launch's groups are read.
 enum : int {
@@ -151,22 +167,16 @@ enum : int {
 // kernel arguments or the registry makes the compiler copy the arguments to
 // private memory.
 template <int kLookup>
-__device__ __forceinline__ gu16* item_factor(const KernelArgs& a, const Item& it, bool shrink) {
-    if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups))
-        return (gu16*)a.gfac[2 * it.group + (shrink ? 0 : 1)];
-    const DevAdapter* d = a.table + it.adapter;
-    return (gu16*)(shrink ? d->A : d->B);
-}
-template <int kLookup>
-__device__ __forceinline__ float item_scale(const KernelArgs& a, const Item& it) {
-    if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups))
-        return a.gscale[it.group];
-    return a.table[it.adapter].scale;
-}
-template <int kLookup>
 __device__ __forceinline__ void resolve(const KernelArgs& a, Item& it) {
-    it.fac = (const void*)item_factor<kLookup>(a, it, it.kind == kItemShrink);
-    it.scale = item_scale<kLookup>(a, it);
+    const bool shrink = it.kind == kItemShrink;
+    if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups)) {
+        it.fac = a.gfac[2 * it.group + (shrink ? 0 : 1)];
+        it.scale = a.gscale[it.group];
+    } else {
+        const DevAdapter* d = a.table + it.adapter;
+        it.fac = shrink ? d->A : d->B;
+        it.scale = d->scale;
+    }
 }
 
 // The launch's factor pointers and scales, striped over a wave's lanes: lane
@@ -178,14 +188,21 @@ struct LaneTable {
     float s[2];
 };
 static_assert(2 * kKargGroups == 4 * 64 && kKargGroups == 2 * 64, "lane table shape");
-__device__ __forceinline__ LaneTable load_lane_table(const KernelArgs& a) {
+// The table is read through the kernel argument segment (the step kernel's
+// KernelArgs follow its 8-byte item pointer), not through the by-value
+// parameter: a lane-dependent index into the parameter can make the compiler
+// copy the whole argument block to private memory.
+static_assert(alignof(KernelArgs) == 8, "step kernel arguments: KernelArgs at offset 8");
+__device__ __forceinline__ LaneTable load_lane_table() {
     const int l = threadIdx.x & 63;
-    const uint64_t* g = reinterpret_cast<const uint64_t*>(a.gfac);
+    const unsigned char* kp = (const unsigned char*)__builtin_amdgcn_kernarg_segment_ptr() + 8;
+    const uint64_t* g = (const uint64_t*)(kp + offsetof(KernelArgs, gfac));
+    const float* sc = (const float*)(kp + offsetof(KernelArgs, gscale));
     LaneTable t;
 #pragma unroll
     for (int i = 0; i < 4; ++i) t.f[i] = g[l + 64 * i];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) t.s[i] = a.gscale[l + 64 * i];
+    for (int i = 0; i < 2; ++i) t.s[i] = sc[l + 64 * i];
     return t;
 }
 __device__ __forceinline__ void resolve_lanes(const LaneTable& t, Item& it) {
@@ -227,109 +244,114 @@ __device__ __forceinline__ int row_of(int rowv, int r) {
     return __builtin_amdgcn_ds_bpermute(r << 2, rowv);
 }
 
-// Partial-block stores and loads: plain, or device-coherent (agent scope) in
-// the step launch, where producer and consumer may sit on different XCDs.
-template <bool kSync>
-__device__ __forceinline__ void put_f32(float* p, float v) {
-    if constexpr (kSync) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else *p = v;
+// ---------------------------------------------------------------------------
+// Buffer operations.  A buffer resource covers [base, base + bytes); a load
+// at an offset past bytes returns zeros and a store there is dropped, so a
+// masked lane is an out-of-range offset, not a branch.  Every buffer this
+// library builds spans less than kMaxSpan bytes, so kOut is past all of them.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data format
+constexpr int kOut = 0x7fffff00;
+constexpr int kCoherent = 16;            // cache policy sc1: device-coherent (agent scope) access
+static_assert((uint32_t)kOut > kMaxSpan, "out-of-range offset");
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
 }
-template <bool kSync>
-__device__ __forceinline__ void put_f32x4(float* p, const f32x4& v) {   // p 16-byte aligned
-    if constexpr (kSync) {
-        const uint64_t lo = (uint64_t)__float_as_uint(v[0]) | ((uint64_t)__float_as_uint(v[1]) << 32);
-        const uint64_t hi = (uint64_t)__float_as_uint(v[2]) | ((uint64_t)__float_as_uint(v[3]) << 32);
-        __hip_atomic_store((uint64_t*)p, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store((uint64_t*)p + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-        *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
-    }
+template <int AUX = 0>
+__device__ __forceinline__ u32x4 bload16(rsrc_t r, int off) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
 }
-template <bool kSync>
-__device__ __forceinline__ float get_f32(const float* p) {
-    if constexpr (kSync) return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else return *p;
+template <int AUX = 0>
+__device__ __forceinline__ u32x2 bload8(rsrc_t r, int off) {
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX));
+}
+template <int AUX = 0>
+__device__ __forceinline__ void bstore16(const u32x4& v, rsrc_t r, int off) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, AUX);
 }
 
-// Step launch: between launches the partial blocks hold this bit pattern, a
-// NaN whose low payload bits no 16-bit input can carry into a float32 sum.
+__device__ __forceinline__ u32x4 as_u4(const f32x4& v) { return __builtin_bit_cast(u32x4, v); }
+__device__ __forceinline__ f32x4 as_f4(const u32x4& v) { return __builtin_bit_cast(f32x4, v); }
+
+// Step launch: between launches the partial and v blocks hold this bit
+// pattern, a NaN whose low payload bits no 16-bit input can carry into a
+// float32 sum.
 constexpr uint32_t kSentinel = 0xffffffffu;
-__device__ __forceinline__ bool unready(float v) { return __float_as_uint(v) == kSentinel; }
-
-// Part q of the ordered sums of a row block's partial blocks at two positions
-// (two consecutive ranks): blocks q, q+P, q+2P, ... added in that order,
-// sixteen loads in flight.  In the step launch a value that still holds the
-// sentinel has not been written yet and is loaded again; budget is the
-// thread's remaining polling rounds (spin_limit for the whole item): once it
-// is spent the status flag is raised and values are used as they are.
-template <bool kSync>
-__device__ __forceinline__ float2 part_sum2(const KernelArgs& a, const float* src0, const float* src1,
-                                            int64_t pstride, int nsplit, int P, int q, bool ok0, bool ok1,
-                                            int& budget) {
-    float s0 = 0.f, s1 = 0.f;
-    for (int c0 = q; c0 < nsplit; c0 += 8 * P) {
-        float u[8], w[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int c = c0 + i * P;
-            const int64_t off = (int64_t)c * pstride;
-            u[i] = (ok0 && c < nsplit) ? get_f32<kSync>(src0 + off) : 0.f;
-            w[i] = (ok1 && c < nsplit) ? get_f32<kSync>(src1 + off) : 0.f;
-        }
-        if constexpr (kSync) {
-            for (;;) {
-                bool miss = false;
-#pragma unroll
-                for (int i = 0; i < 8; ++i) miss |= unready(u[i]) | unready(w[i]);
-                if (!miss || budget < 0) break;
-                if (budget-- == 0) {
-                    __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {     // only positions that were loaded can hold the sentinel
-                    const int64_t off = (int64_t)(c0 + i * P) * pstride;
-                    if (unready(u[i])) u[i] = get_f32<true>(src0 + off);
-                    if (unready(w[i])) w[i] = get_f32<true>(src1 + off);
-                }
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s0 += u[i];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s1 += w[i];
-    }
-    return make_float2(s0, s1);
+__device__ __forceinline__ bool unready4(const u32x4& v) {
+    return (v.x == kSentinel) | (v.y == kSentinel) | (v.z == kSentinel) | (v.w == kSentinel);
 }
 
-// The same ordered sum at one position (the reduce kernel's).
-__device__ __forceinline__ float part_sum(const float* src, int64_t pstride, int nsplit, int P, int q) {
-    float s = 0.f;
-    for (int c0 = q; c0 < nsplit; c0 += 8 * P) {
-        float u[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int c = c0 + i * P;
-            u[i] = c < nsplit ? src[(int64_t)c * pstride] : 0.f;
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s += u[i];
+// Step launch: wait until none of the N 16-byte values v[i] (loaded from r at
+// off[i]; masked ones read zeros) holds the sentinel, reloading those that
+// do.  budget is the thread's remaining polling rounds; once it is spent the
+// status flag is raised and values are used as they are.  (Compile-time
+// recursion over the values: the indices stay constants.)
+template <int I, int N>
+__device__ __forceinline__ bool any_unready(const u32x4 (&v)[N]) {
+    if constexpr (I < N) return unready4(v[I]) || any_unready<I + 1, N>(v);
+    return false;
+}
+template <int I, int N>
+__device__ __forceinline__ void reload_unready(u32x4 (&v)[N], rsrc_t r, const int (&off)[N]) {
+    if constexpr (I < N) {
+        if (unready4(v[I])) v[I] = bload16<kCoherent>(r, off[I]);
+        reload_unready<I + 1, N>(v, r, off);
     }
-    return s;
+}
+template <int N>
+__device__ __forceinline__ void poll16(const KernelArgs& a, u32x4 (&v)[N], rsrc_t r, const int (&off)[N],
+                                       int& budget) {
+    while (any_unready<0, N>(v) && budget >= 0) {
+        if (budget-- == 0) {
+            __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        reload_unready<0, N>(v, r, off);
+    }
 }
 
 // Step launch: the row block's two partial buffers.  Launches alternate
 // between them, the parity coming from the row block's counter of finished
 // expand items (it wraps at 2 nexp): below nexp -> buffer 0, else buffer 1.
-// Within one launch every reader sees the same parity: all shrink items of a
-// row block start before any of its expand items can finish, and an expand
-// item that reads late sees fewer than nexp increments of its own launch.
-// Each shrink item arms (sets to the sentinel) its block in the buffer the
-// next launch will use, which no item of this launch reads.
+// Within one launch every reader sees the same parity: every shrink and
+// reduce item of a row block starts before any of its expand items can
+// finish, and an expand item that reads late sees fewer than nexp increments
+// of its own launch.  Each producer arms (sets to the sentinel) its block in
+// the buffer the next launch will use, which no item of this launch reads.
+// Read before the item's other loads: vector loads complete in order, so a
+// wait for this one then waits for nothing else.
 __device__ __forceinline__ uint32_t row_block_parity(const KernelArgs& a, const Item& it) {
     const uint32_t c = __hip_atomic_load(a.sync + (int64_t)it.rb * kSyncStride, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return c >= (uint32_t)it.nexp ? 1u : 0u;
+}
+
+// The 8 x 8 transpose of 16-bit values: in[k] holds 8 consecutive elements
+// of row k; out[c] gets element c of rows 0..7 (row k at position k).
+__device__ __forceinline__ void transpose8x8(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const int w = c >> 1;
+        u32x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t a = in[2 * q][w], b = in[2 * q + 1][w];
+            o[q] = (c & 1) ? pack_hi(a, b) : pack_lo(a, b);
+        }
+        out[c] = o;
+    }
+}
+// The 4 x 4 transpose: in[k] holds 4 consecutive elements of row k; out[c]
+// gets element c of rows 0..3.
+__device__ __forceinline__ void transpose4x4(const u32x2 (&in)[4], u32x2 (&out)[4]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int w = c >> 1;
+        out[c] = (c & 1) ? u32x2{pack_hi(in[0][w], in[1][w]), pack_hi(in[2][w], in[3][w])}
+                         : u32x2{pack_lo(in[0][w], in[1][w]), pack_lo(in[2][w], in[3][w])};
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -342,105 +364,94 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     const int w = t >> 6;
     const int lr = t & 15;
     const int lg = (t >> 4) & 3;
+    uint32_t parity = 0;                      // step launch: which partial buffer (read first, used last)
+    if constexpr (kSync) parity = row_block_parity(a, it);
     const int R = it.rank;
     const int Rp = round_up_i(R, 16);
+    const int Rv = rank_stride(R);
     const int NT = Rp / 16;
     const int sub = it.sub;                   // K staged per pass, multiple of 32
-    const int KP = shrink_kp(sub);            // words per A^T row, 4 (mod 8): conflict-free 16-byte reads
-    const int KX = shrink_kx(sub);            // halves per x row
+    const int KC = shrink_chunks(sub);        // 16-byte chunks per LDS row (odd)
+    const int nk8 = sub / 8;
     const int nrows = it.nrows;
     const int WN = shrink_wn(R);
     const int WK = 4 / WN;
     const int wn = w % WN;
     const int wk = w / WN;
-    uint32_t* As = (uint32_t*)smem;                               // [Rp][KP] words
-    uint16_t* Xs = (uint16_t*)(smem + (size_t)Rp * KP * 4);       // [MS*16][KX]
-    gu16* A = (gu16*)it.fac + (int64_t)it.lo * R;
-    const uint16_t* X = (const uint16_t*)a.x + it.lo;
+    u32x4* As = (u32x4*)smem;                 // [Rp][KC] chunks of A^T (8 consecutive K of one rank)
+    u32x4* Xs = As + Rp * KC;                 // [MS*16][KC] chunks of x
+    const rsrc_t ar = make_rsrc((const uint16_t*)it.fac + (int64_t)it.lo * R, (uint32_t)it.len * R * 2);
+    const rsrc_t xr = make_rsrc(a.x, a.x_bytes);
     const int rowv = lane_rows(a, it);
     const u32x4 z4 = {0u, 0u, 0u, 0u};
     const bool vec = (R & 7) == 0;
-    const int VPR = max_i(R / 8, 1);
-    const int npairs = vec ? (sub / 2) * VPR : 0;
-    const int kv = sub / 8;
-    const int nx = nrows * kv;
+    // A transpose unit of this thread: eight K rows (8 k8 .. 8 k8 + 7) of ranks
+    // 8 jo .. 8 jo + 7.  Eight consecutive lanes take eight consecutive k8 of
+    // one jo (their 16-byte LDS writes hit distinct banks); a wave covers whole
+    // rows of A.
+    const int VPR = vec ? R / 8 : 1;
+    const int rest = t >> 3;
+    const int jo = rest % VPR;
+    const int k8 = (t & 7) + 8 * (rest / VPR);
+    const bool aunit = vec && rest < VPR * (32 / VPR) && k8 < nk8;
+    const int aoff0 = (8 * k8 * R + 8 * jo) * 2;   // bytes, pass start excluded
+    // x chunks of this thread: chunk c of row r, p = t + 256 i
+    int xoff[4], xc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int p = t + i * kThreads;
+        const int r = p / nk8;
+        xc[i] = p - r * nk8;
+        const int row = row_of(rowv, r < nrows ? r : 0);
+        xoff[i] = r < nrows ? (int)(((int64_t)row * a.ldx + it.lo + 8 * xc[i]) * 2) : kOut;
+    }
     const int npass = (it.len + sub - 1) / sub;
-    uint32_t parity = 0;                       // step launch: which partial buffer (read early, used last)
-    if constexpr (kSync) parity = row_block_parity(a, it);
 
     // the padding ranks of A^T stay zero for every pass
-    for (int i = t; i < (Rp - R) * KP; i += kThreads) As[R * KP + i] = 0u;
+    for (int i = t; i < (Rp - (vec ? R : 0)) * KC; i += kThreads) As[(vec ? R : 0) * KC + i] = z4;
 
-    u32x4 v0[4], v1[4], xv[4];
-    auto load_pass = [&](int pass) {
+    u32x4 av[8], xv[4];
+    auto load_pass = [&](int pass) __attribute__((always_inline)) {
         const int k0 = pass * sub;
         const int plen = min_i(sub, it.len - k0);
-        const int lv = plen / 8;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = t + i * kThreads;
-            const int k2 = p / VPR;
-            const int k = 2 * k2;
-            const int jo = p - k2 * VPR;
-            const bool ok0 = p < npairs && k < plen;
-            const bool ok1 = p < npairs && k + 1 < plen;
-            // addresses stay inside A even where the load is masked off
-            gu16* src0 = A + (int64_t)(ok0 ? k0 + k : 0) * R + (ok0 ? jo * 8 : 0);
-            gu16* src1 = A + (int64_t)(ok1 ? k0 + k + 1 : 0) * R + (ok1 ? jo * 8 : 0);
-            v0[i] = ok0 ? *(gu32x4*)src0 : z4;
-            v1[i] = ok1 ? *(gu32x4*)src1 : z4;
+        for (int kk = 0; kk < 8; ++kk) {
+            const bool ok = aunit && 8 * k8 + kk < plen;
+            av[kk] = bload16(ar, ok ? aoff0 + ((k0 + kk) * R) * 2 : kOut);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = t + i * kThreads;
-            const int r = p < nx ? p / kv : 0;
-            const int c = p - r * kv;
-            const int row = row_of(rowv, r);
-            const bool ok = p < nx && c < lv;
-            xv[i] = ok ? *(const u32x4*)(X + (int64_t)row * a.ldx + k0 + (ok ? c * 8 : 0)) : z4;
-        }
+        for (int i = 0; i < 4; ++i) xv[i] = bload16(xr, 8 * xc[i] < plen && xoff[i] != kOut ? xoff[i] + 2 * k0 : kOut);
     };
-    auto store_x = [&]() {
+    auto store_x = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int p = t + i * kThreads;
-            if (p < nx) {
-                const int r = p / kv;
-                *(u32x4*)(Xs + r * KX + (p - r * kv) * 8) = xv[i];
+            if (p < MS * 16 * nk8) {
+                const int r = p / nk8;
+                Xs[r * KC + (p - r * nk8)] = xv[i];    // rows >= nrows: zero
             }
         }
     };
-    auto store_a = [&]() {
+    auto store_a = [&]() __attribute__((always_inline)) {
+        if (aunit) {
+            u32x4 o[8];
+            transpose8x8(av, o);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = t + i * kThreads;
-            if (p < npairs) {
-                const int k2 = p / VPR;
-                const int jo = p - k2 * VPR;
-                uint32_t* d = As + (jo * 8) * KP + k2;
-                d[0 * KP] = lo16(v0[i].x) | (v1[i].x << 16);
-                d[1 * KP] = hi16(v0[i].x) | (v1[i].x & 0xffff0000u);
-                d[2 * KP] = lo16(v0[i].y) | (v1[i].y << 16);
-                d[3 * KP] = hi16(v0[i].y) | (v1[i].y & 0xffff0000u);
-                d[4 * KP] = lo16(v0[i].z) | (v1[i].z << 16);
-                d[5 * KP] = hi16(v0[i].z) | (v1[i].z & 0xffff0000u);
-                d[6 * KP] = lo16(v0[i].w) | (v1[i].w << 16);
-                d[7 * KP] = hi16(v0[i].w) | (v1[i].w & 0xffff0000u);
-            }
+            for (int c = 0; c < 8; ++c) As[(8 * jo + c) * KC + k8] = o[c];
         }
     };
     // ranks that are not a multiple of 8: A^T element by element (correct, not tuned)
-    auto store_a_generic = [&](int pass) {
+    auto store_a_generic = [&](int pass) __attribute__((always_inline)) {
         const int k0 = pass * sub;
         const int plen = min_i(sub, it.len - k0);
-        for (int i = t; i < R * KP; i += kThreads) As[i] = 0u;
+        for (int i = t; i < R * KC; i += kThreads) As[i] = z4;
         __syncthreads();
         uint16_t* As16 = (uint16_t*)As;
-        gu16* src = A + (int64_t)k0 * R;
+        gu16* src = (gu16*)it.fac + ((int64_t)it.lo + k0) * R;
         for (int e = t; e < plen * R; e += kThreads) {
             const int k = e / R;
             const int j = e - k * R;
-            As16[(j * KP) * 2 + k] = src[e];
+            As16[j * KC * 8 + k] = src[e];
         }
     };
 
@@ -463,19 +474,17 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
         // U K-steps per round: every fragment of the round is read from LDS
         // before its MFMAs, so the reads overlap instead of each MFMA waiting
         // for its own
-        auto step_frags = [&](int s, u32x4 (&af)[TQ], u32x4 (&xf)[MS]) {
+        auto step_frags = [&](int s, u32x4 (&af)[TQ], u32x4 (&xf)[MS]) __attribute__((always_inline)) {
 #pragma unroll
             for (int q = 0; q < TQ; ++q) {
                 const int tile = wn + WN * q;
-                af[q] = tile < NT ? *(const u32x4*)(As + (tile * 16 + lr) * KP + 16 * s + 4 * lg) : z4;
+                af[q] = As[((tile < NT ? tile : 0) * 16 + lr) * KC + 4 * s + lg];
+                if (tile >= NT) af[q] = z4;
             }
 #pragma unroll
-            for (int m = 0; m < MS; ++m) {
-                const int row = m * 16 + lr;
-                xf[m] = row < nrows ? *(const u32x4*)(Xs + row * KX + 32 * s + 8 * lg) : z4;
-            }
+            for (int m = 0; m < MS; ++m) xf[m] = Xs[(m * 16 + lr) * KC + 4 * s + lg];
         };
-        auto step_mma = [&](const u32x4 (&af)[TQ], const u32x4 (&xf)[MS]) {
+        auto step_mma = [&](const u32x4 (&af)[TQ], const u32x4 (&xf)[MS]) __attribute__((always_inline)) {
 #pragma unroll
             for (int m = 0; m < MS; ++m)
 #pragma unroll
@@ -497,9 +506,10 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
         }
     }
 
-    // lane holds v[row m*16+lr][ranks tile*16 + 4lg .. +3]
-    float* part = a.partials + it.part;
-    if constexpr (kSync) part += parity ? a.pbuf : 0;
+    // lane holds v[row m*16+lr][ranks tile*16 + 4lg .. +3]; the partial block
+    // is [nrows][Rv] (ranks R..Rv-1 hold the zeros of the padded A^T)
+    const float* pbase = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
+    const rsrc_t pr = make_rsrc(pbase, (uint32_t)it.pstride * 4);
     if (WK == 1) {
 #pragma unroll
         for (int m = 0; m < MS; ++m) {
@@ -507,50 +517,41 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
             for (int q = 0; q < TQ; ++q) {
                 const int tile = wn + WN * q;
                 const int row = m * 16 + lr;
-                if (tile < NT && row < nrows) {
-                    const int r0 = tile * 16 + 4 * lg;
-                    float* dst = part + row * R + r0;
-                    if ((R & 3) == 0 && r0 + 3 < R) {
-                        put_f32x4<kSync>(dst, acc[m][q]);
-                    } else {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            if (r0 + i < R) put_f32<kSync>(dst + i, acc[m][q][i]);
-                    }
-                }
+                const int r0 = tile * 16 + 4 * lg;
+                const bool ok = tile < NT && row < nrows && r0 < Rv;
+                bstore16<kSync ? kCoherent : 0>(as_u4(acc[m][q]), pr, ok ? (row * Rv + r0) * 4 : kOut);
             }
         }
     } else {
         __syncthreads();                      // staging is read no more
-        float* red = (float*)smem;            // [WK][MS*16][Rp]
+        float* red = (float*)smem;            // [WK][MS*16][Rp + 4]
+        const int RS = Rp + 4;
 #pragma unroll
         for (int m = 0; m < MS; ++m) {
 #pragma unroll
             for (int q = 0; q < TQ; ++q) {
                 const int tile = wn + WN * q;
                 if (tile < NT)
-                    *(float4*)(red + ((wk * MS + m) * 16 + lr) * Rp + tile * 16 + 4 * lg) =
-                        make_float4(acc[m][q][0], acc[m][q][1], acc[m][q][2], acc[m][q][3]);
+                    *(f32x4*)(red + ((wk * MS + m) * 16 + lr) * RS + tile * 16 + 4 * lg) = acc[m][q];
             }
         }
         __syncthreads();
-        for (int o = t; o < nrows * R; o += kThreads) {
-            const int row = o / R;
-            const int rank = o - row * R;
-            float s = red[row * Rp + rank];
-            for (int k = 1; k < WK; ++k) s += red[(k * MS * 16 + row) * Rp + rank];
-            put_f32<kSync>(part + o, s);
+        const int n4 = nrows * Rv / 4;
+        for (int o = t; o < n4; o += kThreads) {
+            const int row = (4 * o) / Rv;
+            const int r0 = 4 * o - row * Rv;
+            f32x4 sum = *(const f32x4*)(red + row * RS + r0);
+            for (int k = 1; k < WK; ++k) sum += *(const f32x4*)(red + (k * MS * 16 + row) * RS + r0);
+            bstore16<kSync ? kCoherent : 0>(as_u4(sum), pr, 16 * o);
         }
     }
     if constexpr (kSync) {
-        // arm this block in the other buffer for the next launch, after this
-        // launch's block is out.  Plain stores: only the next launch reads
-        // them, and a kernel's end makes its stores visible to the next.  The
-        // block is reserved to a multiple of 4 floats, so whole 16-byte
-        // stores stay inside it.
-        u32x4* other = (u32x4*)(a.partials + (parity ? 0 : a.pbuf) + it.part);
+        // arm this block in the other buffer for the next launch.  Plain
+        // stores: only the next launch reads them, and a kernel's end makes
+        // its stores visible to the next.
+        const rsrc_t orr = make_rsrc(a.partials + it.part + (parity ? 0 : a.pbuf), (uint32_t)it.pstride * 4);
         const u32x4 s4 = {kSentinel, kSentinel, kSentinel, kSentinel};
-        for (int o = t; 4 * o < nrows * R; o += kThreads) other[o] = s4;
+        for (int o = t; 4 * o < it.pstride; o += kThreads) bstore16(s4, orr, 16 * o);
     }
 }
 
@@ -573,211 +574,276 @@ __device__ __forceinline__ void shrink_item(const KernelArgs& a, const Item& it,
     }
 }
 
-// Two workgroups per CU: the register budget is capped at 256 per lane.
 template <class Fmt>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
-lora_shrink_kernel(KernelArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) lora_shrink_kernel(KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kShrinkLds];
-    const Item it = load_item(a.items + blockIdx.x);
+    Item it = load_item(a.items + blockIdx.x);
     if (it.kind != kItemShrink) return;
-    Item r = it;
-    resolve<kLookupAuto>(a, r);
-    shrink_item<Fmt, false>(a, r, smem);
+    resolve<kLookupAuto>(a, it);
+    shrink_item<Fmt, false>(a, it, smem);
+}
+
+// ---------------------------------------------------------------------------
+// Reduce: floats [lo, lo + len) of the row block's v block (len a multiple
+// of 4) are the sum of its nsplit partial blocks.  Thread (position p, group
+// q) adds blocks q, q + G, q + 2G, ... in order (G = sub split groups, at
+// most kMaxSplitLoads blocks per thread, all loads in flight together); the G
+// sums are then added in order q = 0..G-1.  The order depends on the plan
+// only, so every launch form adds identically.  With a caller v (lora_shrink)
+// the sums go to its rows instead of the v block.
+// ---------------------------------------------------------------------------
+template <bool kSync>
+__device__ __forceinline__ void reduce_body(const KernelArgs& a, const Item& it, unsigned char* smem) {
+    const int t = threadIdx.x;
+    uint32_t parity = 0;
+    if constexpr (kSync) parity = row_block_parity(a, it);
+    const int Rv = rank_stride(it.rank);
+    const int np = it.len / 4;                // float4 positions of the slice
+    const int G = it.sub;
+    const int p = t % np;
+    const int q = t / np;
+    f32x4* red = (f32x4*)smem;                // [G][np]
+    const float* P = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
+    const rsrc_t pr = make_rsrc(P, (uint32_t)(it.nsplit + 1) * it.pstride * 4);
+    int budget = a.spin_limit;
+    if (q < G) {
+        int off[kMaxSplitLoads];
+        u32x4 u[kMaxSplitLoads];
+#pragma unroll
+        for (int i = 0; i < kMaxSplitLoads; ++i) {
+            const int c = q + i * G;
+            off[i] = c < it.nsplit ? (c * it.pstride + it.lo + 4 * p) * 4 : kOut;
+            u[i] = bload16<kSync ? kCoherent : 0>(pr, off[i]);
+        }
+        if constexpr (kSync) poll16<kMaxSplitLoads>(a, u, pr, off, budget);
+        f32x4 s = as_f4(u[0]);
+#pragma unroll
+        for (int i = 1; i < kMaxSplitLoads; ++i) s += as_f4(u[i]);
+        red[q * np + p] = s;
+    }
+    __syncthreads();
+    if (t < np) {
+        f32x4 s = red[t];
+        for (int g = 1; g < G; ++g) s += red[g * np + t];
+        const int f = it.lo + 4 * t;          // flat index in the v block
+        if (a.v) {
+            const int row = f / Rv;
+            const int r0 = f - row * Rv;
+            float* dst = a.v + (int64_t)a.perm[it.p0 + row] * a.ldv + r0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (r0 + i < it.rank) dst[i] = s[i];
+        } else {
+            const int vo = (it.nsplit * it.pstride + f) * 4;
+            bstore16<kSync ? kCoherent : 0>(as_u4(s), pr, vo);
+            if constexpr (kSync) {
+                // arm this slice in the other buffer for the next launch
+                const rsrc_t orr = make_rsrc(a.partials + it.part + (parity ? 0 : a.pbuf),
+                                             (uint32_t)(it.nsplit + 1) * it.pstride * 4);
+                bstore16(u32x4{kSentinel, kSentinel, kSentinel, kSentinel}, orr, vo);
+            }
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kThreads) lora_reduce_kernel(KernelArgs a) {
+    __shared__ __attribute__((aligned(16))) unsigned char smem[kReduceLds];
+    const Item it = load_item(a.items + blockIdx.x);
+    if (it.kind != kItemReduce) return;
+    reduce_body<false>(a, it, smem);
 }
 
 // ---------------------------------------------------------------------------
 // Expand
 // ---------------------------------------------------------------------------
-template <class Fmt, int Q, int MS, bool kSync>
+// Column order inside a 64-column block: MFMA output row m of instruction c
+// (c = 0..3) is column base(m) + c.  A lane then loads 4 consecutive columns
+// of B (sixteen lanes: one 128-byte row segment) and ends up holding columns
+// 8g .. 8g+7 and 32 + 8g .. 32 + 8g + 7 of its row (g = lane / 16).
+__device__ __forceinline__ int col_base(int m) { return 8 * (m >> 2) + 32 * ((m >> 1) & 1) + 4 * (m & 1); }
+
+template <class Fmt, int Q, int KSG, int MS, bool kSync>
 __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                                             unsigned char* smem) {
     const int t = threadIdx.x;
     const int w = t >> 6;
-    const int lr = t & 15;
-    const int lg = (t >> 4) & 3;
+    const int l = t & 63;
+    const int lr = l & 15;
+    const int lg = l >> 4;
+    uint32_t parity = 0;                      // step launch (read first, see row_block_parity)
+    if constexpr (kSync) parity = row_block_parity(a, it);
     const int R = it.rank;
-    const int Rk = round_up_i(R, 16);
-    const int KS = Rk / 16;
-    const int half = Rk / 2;
-    const int RP = expand_rp(R);              // words per row: two ranks each, 2 (mod 4)
+    const int Rv = rank_stride(R);
+    const int KS = round_up_i(R, 16) / 16;
     const int len = it.len;
-    const int ncol = round_up_i(len, 16);
-    const int NCT = ncol / 16;
     const int nrows = it.nrows;
-    uint32_t* Bs = (uint32_t*)smem;           // [ncol][RP]  B^T, rank pairs
-    uint32_t* Vh = Bs + ncol * RP;            // [MS*16][RP]  high part of v
-    uint32_t* Vl = Vh + MS * 16 * RP;         // [MS*16][RP]  low part of v
-    float2* red = (float2*)(Vl + MS * 16 * RP);   // [kThreads]
-    gu16* B = (gu16*)it.fac;
+    const int h_out = a.h_out;
+    u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v (high | low part)
+    const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
+    const rsrc_t br = make_rsrc((const uint16_t*)it.fac + it.lo, (uint32_t)(R * h_out - it.lo) * 2);
     const float scale = it.scale;
     const int rowv = lane_rows(a, it);
-    const u32x4 z4 = {0u, 0u, 0u, 0u};
 
-    // --- requests: the B tile (<= 4 rank-pair loads per thread by the tiling) ...
-    const int cv = ncol / 8;                  // column octets
-    const int npairs = half * cv;
-    u32x4 b0[4], b1[4];
+    // --- this lane's y: rows m*16+lr, columns cb*64 + 32h + 8lg .. +7 of the
+    // wave's column blocks cb = w + 4q
+    int yoff[Q][MS][2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int p = t + i * kThreads;
-        const int jp = p / cv;
-        const int co = p - jp * cv;
-        const int j = 2 * jp;
-        const bool ok0 = p < npairs && co * 8 < len && j < R;
-        const bool ok1 = p < npairs && co * 8 < len && j + 1 < R;
-        // addresses stay inside B even where the load is masked off
-        gu16* src0 = B + (int64_t)(ok0 ? j : 0) * a.h_out + it.lo + (ok0 ? co * 8 : 0);
-        gu16* src1 = B + (int64_t)(ok1 ? j + 1 : 0) * a.h_out + it.lo + (ok1 ? co * 8 : 0);
-        b0[i] = ok0 ? *(gu32x4*)src0 : z4;
-        b1[i] = ok1 ? *(gu32x4*)src1 : z4;
-    }
-    // ... this lane's y: rows m*16+lr, columns ct*16 + 4lg .. +3 of the wave's
-    // column tiles ct = w, w+4, ...
-    int yrow[MS];
+    for (int m = 0; m < MS; ++m) {
+        const int row = row_of(rowv, m * 16 + lr < nrows ? m * 16 + lr : 0);
 #pragma unroll
-    for (int m = 0; m < MS; ++m) yrow[m] = row_of(rowv, m * 16 + lr < nrows ? m * 16 + lr : 0);
-    u32x2 yv[Q][MS];
+        for (int q = 0; q < Q; ++q)
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-        const int ct = w + 4 * q;
-        const int c = ct * 16 + 4 * lg;
-#pragma unroll
-        for (int m = 0; m < MS; ++m) {
-            const bool ok = ct < NCT && m * 16 + lr < nrows && c + 4 <= len;
-            const uint16_t* src = (const uint16_t*)a.y + (int64_t)yrow[m] * a.ldy + it.lo + (ok ? c : 0);
-            yv[q][m] = ok ? *(const u32x2*)src : u32x2{0u, 0u};
-        }
-    }
-    // ... and v: rank pairs of every row, the sum of the row block's partial
-    // blocks (or the caller's v).  With few slots, P threads share a slot,
-    // each adding every P-th block; the P sums are then added in order.
-    const int slots = nrows * half;
-    const int nslot = MS * 16 * half;
-    const int P = a.v ? 1 : partial_parts(nrows, R, it.nsplit);
-    const float* Pb = a.partials + it.part;
-    if constexpr (kSync) Pb += row_block_parity(a, it) ? a.pbuf : 0;
-    int budget = a.spin_limit;                // step launch: polling rounds left to this thread
-    auto sum_parts = [&]() {
-        if (P > 1) {
-            const int slot = t % slots;
-            const int q = t / slots;
-            if (q < P) {
-                const int row = slot / half;
-                const int j = 2 * (slot - row * half);
-                const float* src = Pb + row * R;
-                red[t] = part_sum2<kSync>(a, src + (j < R ? j : 0), src + (j + 1 < R ? j + 1 : 0), it.pstride,
-                                          it.nsplit, P, q, j < R, j + 1 < R, budget);
+            for (int h = 0; h < 2; ++h) {
+                const int c = (w + 4 * q) * 64 + 32 * h + 8 * lg;
+                const bool ok = m * 16 + lr < nrows && c + 8 <= len;
+                yoff[q][m][h] = ok ? (int)(((int64_t)row * a.ldy + it.lo + c) * 2) : kOut;
             }
-        }
-    };
-    // --- B^T to LDS
-    auto store_bt = [&]() {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int p = t + i * kThreads;
-            if (p < npairs) {
-                const int jp = p / cv;
-                const int co = p - jp * cv;
-                uint32_t* d = Bs + (co * 8) * RP + jp;
-                d[0 * RP] = lo16(b0[i].x) | (b1[i].x << 16);
-                d[1 * RP] = hi16(b0[i].x) | (b1[i].x & 0xffff0000u);
-                d[2 * RP] = lo16(b0[i].y) | (b1[i].y << 16);
-                d[3 * RP] = hi16(b0[i].y) | (b1[i].y & 0xffff0000u);
-                d[4 * RP] = lo16(b0[i].z) | (b1[i].z << 16);
-                d[5 * RP] = hi16(b0[i].z) | (b1[i].z & 0xffff0000u);
-                d[6 * RP] = lo16(b0[i].w) | (b1[i].w << 16);
-                d[7 * RP] = hi16(b0[i].w) | (b1[i].w & 0xffff0000u);
-            }
-        }
-    };
-    if constexpr (kSync) {
-        // the B tile and y are requested and B^T staged before the partial
-        // blocks are polled
-        store_bt();
-        sum_parts();
-    } else {
-        sum_parts();
-        store_bt();
     }
-    if (P > 1) __syncthreads();               // the P-way sums are in red
-    // --- v to LDS as high / low 16-bit parts (rows past nrows: zero)
-    for (int o = t; o < nslot; o += kThreads) {
-        const int row = o / half;
-        const int jp = o - row * half;
-        const int j = 2 * jp;
-        float v0 = 0.f, v1 = 0.f;
-        if (row < nrows) {
-            if (a.v) {
-                const float* src = a.v + (int64_t)a.perm[it.p0 + row] * a.ldv;
-                if (j < R) v0 = src[j];
-                if (j + 1 < R) v1 = src[j + 1];
-            } else if (P > 1) {
-                for (int q = 0; q < P; ++q) {
-                    const float2 r2 = red[q * slots + o];
-                    v0 += r2.x;
-                    v1 += r2.y;
-                }
-            } else {
-                const float* src = Pb + row * R;
-                const float2 s2 = part_sum2<kSync>(a, src + (j < R ? j : 0), src + (j + 1 < R ? j + 1 : 0),
-                                                   it.pstride, it.nsplit, 1, 0, j < R, j + 1 < R, budget);
-                v0 += s2.x;
-                v1 += s2.y;
-            }
-        }
-        const uint32_t h0 = Fmt::from_f32(v0), h1 = Fmt::from_f32(v1);
-        const uint32_t l0 = Fmt::from_f32(v0 - Fmt::to_f32(h0));
-        const uint32_t l1 = Fmt::from_f32(v1 - Fmt::to_f32(h1));
-        Vh[row * RP + jp] = h0 | (h1 << 16);
-        Vl[row * RP + jp] = l0 | (l1 << 16);
-    }
-    __syncthreads();
-    // step launch: this item has read its partial values; count it (no wait
-    // for the result)
-    if constexpr (kSync)
-        if (t == 0)
-            (void)__builtin_amdgcn_atomic_inc32(a.sync + (int64_t)it.rb * kSyncStride, 2u * (uint32_t)it.nexp - 1u, __ATOMIC_RELAXED,
-                                                "agent");
-
-    // --- y^T = B^T v^T on MFMA, then y + s*d rounded once
-    f32x4 acc[Q][MS];
+    u32x4 yv[Q][MS][2];
 #pragma unroll
     for (int q = 0; q < Q; ++q)
 #pragma unroll
-        for (int m = 0; m < MS; ++m) acc[q][m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < KS; ++s) {
-        u32x2 af[Q];
+        for (int m = 0; m < MS; ++m)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) yv[q][m][h] = bload16(yr, yoff[q][m][h]);
+
+    // --- B: for column block q and rank step ks, lane (lr, lg) loads rows
+    // 16ks + 4lg .. +3, columns cb*64 + base(lr) .. +3
+    const int mycol = col_base(lr);
+    u32x2 bv[Q][KSG][4];
+    auto load_group = [&](int g0) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
-            const int ct = w + 4 * q;
-            af[q] = ct < NCT ? *(const u32x2*)(Bs + (ct * 16 + lr) * RP + 8 * s + 2 * lg) : u32x2{0u, 0u};
+            const int col = (w + 4 * q) * 64 + mycol;
+#pragma unroll
+            for (int kl = 0; kl < KSG; ++kl)
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    const int j = 16 * (g0 + kl) + 4 * lg + kk;
+                    const bool ok = j < R && col + 4 <= len;
+                    bv[q][kl][kk] = bload8(br, ok ? (j * h_out + col) * 2 : kOut);
+                }
         }
+    };
+    load_group(0);
+
+    // --- v fragments to LDS: entry (m, ks, lane) = v[row m*16 + lane%16][ranks
+    // 16ks + 4(lane/16) .. +3] as high and low 16-bit parts
+    {
+        const bool direct = it.sub != 0;      // add the partial blocks up here
+        const float* P = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
+        const rsrc_t pr = make_rsrc(P, (uint32_t)(it.nsplit + 1) * it.pstride * 4);
+        const int vbase = it.nsplit * it.pstride * 4;
+        int budget = a.spin_limit;
+        const int ntask = MS * KS * 64;
+        for (int task = t; task < ntask; task += kThreads) {
+            const int mk = task >> 6;                 // m * KS + ks
+            const int ll = task & 63;
+            const int m = mk / KS;
+            const int ks = mk - m * KS;
+            const int row = m * 16 + (ll & 15);
+            const int j0 = 16 * ks + 4 * (ll >> 4);
+            const bool ok = row < nrows && j0 < R;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (a.v) {
+                if (ok) {
+                    const float* src = a.v + (int64_t)a.perm[it.p0 + row] * a.ldv + j0;
 #pragma unroll
-        for (int m = 0; m < MS; ++m) {
-            const u32x2 bh = *(const u32x2*)(Vh + (m * 16 + lr) * RP + 8 * s + 2 * lg);
-            const u32x2 bl = *(const u32x2*)(Vl + (m * 16 + lr) * RP + 8 * s + 2 * lg);
+                    for (int i = 0; i < 4; ++i)
+                        if (j0 + i < R) v[i] = src[i];
+                }
+            } else if (direct) {
+                const int o = (row * Rv + j0) * 4;
+                int off[kDirectSplits];
+                u32x4 u[kDirectSplits];
 #pragma unroll
-            for (int q = 0; q < Q; ++q) {
-                acc[q][m] = Fmt::mma16(af[q], bh, acc[q][m]);
-                acc[q][m] = Fmt::mma16(af[q], bl, acc[q][m]);
+                for (int c = 0; c < kDirectSplits; ++c) {
+                    off[c] = ok && c < it.nsplit ? c * it.pstride * 4 + o : kOut;
+                    u[c] = bload16<kSync ? kCoherent : 0>(pr, off[c]);
+                }
+                if constexpr (kSync) poll16<kDirectSplits>(a, u, pr, off, budget);
+                v = as_f4(u[0]);
+#pragma unroll
+                for (int c = 1; c < kDirectSplits; ++c) v += as_f4(u[c]);
+            } else {
+                int off[1] = {ok ? vbase + (row * Rv + j0) * 4 : kOut};
+                u32x4 u[1] = {bload16<kSync ? kCoherent : 0>(pr, off[0])};
+                if constexpr (kSync) poll16<1>(a, u, pr, off, budget);
+                v = as_f4(u[0]);
             }
+            u32x4 f;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const float v0 = v[2 * i], v1 = v[2 * i + 1];
+                const uint32_t h0 = Fmt::from_f32(v0), h1 = Fmt::from_f32(v1);
+                f[i] = h0 | (h1 << 16);
+                f[2 + i] = Fmt::from_f32(v0 - Fmt::to_f32(h0)) | (Fmt::from_f32(v1 - Fmt::to_f32(h1)) << 16);
+            }
+            Vf[task] = f;
         }
     }
+    __syncthreads();
+    // step launch: this item has read its v; count it (no wait for the result)
+    if constexpr (kSync)
+        if (t == 0)
+            (void)__builtin_amdgcn_atomic_inc32(a.sync + (int64_t)it.rb * kSyncStride, 2u * (uint32_t)it.nexp - 1u,
+                                                __ATOMIC_RELAXED, "agent");
+
+    // --- y^T = B^T v^T on MFMA, KSG rank steps per group
+    f32x4 acc[Q][4][MS];
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int m = 0; m < MS; ++m) acc[q][c][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int g0 = 0; g0 < KS; g0 += KSG) {
+        if (g0 > 0) load_group(g0);
+        u32x4 vf[KSG][MS];
+#pragma unroll
+        for (int kl = 0; kl < KSG; ++kl)
+#pragma unroll
+            for (int m = 0; m < MS; ++m) {
+                const int ks = g0 + kl < KS ? g0 + kl : KS - 1;
+                vf[kl][m] = Vf[(m * KS + ks) * 64 + l];
+                if (g0 + kl >= KS) vf[kl][m] = u32x4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+            for (int kl = 0; kl < KSG; ++kl) {
+                u32x2 fr[4];
+                transpose4x4(bv[q][kl], fr);
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+#pragma unroll
+                    for (int m = 0; m < MS; ++m) {
+                        acc[q][c][m] = Fmt::mma16(fr[c], vf[kl][m].xy, acc[q][c][m]);
+                        acc[q][c][m] = Fmt::mma16(fr[c], vf[kl][m].zw, acc[q][c][m]);
+                    }
+            }
+    }
+
+    // --- epilogue: lane holds, for instruction c and output row 4lg + i,
+    // column cb*64 + 8lg + 32(i >> 1) + 4(i & 1) + c of row m*16 + lr
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-        const int ct = w + 4 * q;
-        const int c = ct * 16 + 4 * lg;
 #pragma unroll
         for (int m = 0; m < MS; ++m) {
-            if (ct < NCT && m * 16 + lr < nrows && c + 4 <= len) {
-                const u32x2 yo = yv[q][m];
-                const float f0 = fmaf(scale, acc[q][m][0], Fmt::to_f32(lo16(yo.x)));
-                const float f1 = fmaf(scale, acc[q][m][1], Fmt::to_f32(hi16(yo.x)));
-                const float f2 = fmaf(scale, acc[q][m][2], Fmt::to_f32(lo16(yo.y)));
-                const float f3 = fmaf(scale, acc[q][m][3], Fmt::to_f32(hi16(yo.y)));
-                *(u32x2*)((uint16_t*)a.y + (int64_t)yrow[m] * a.ldy + it.lo + c) =
-                    u32x2{Fmt::from_f32(f0) | (Fmt::from_f32(f1) << 16),
-                          Fmt::from_f32(f2) | (Fmt::from_f32(f3) << 16)};
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const u32x4 yo = yv[q][m][h];
+                u32x4 o;
+#pragma unroll
+                for (int e2 = 0; e2 < 4; ++e2) {
+                    // elements e = 2 e2, 2 e2 + 1: i = 2h + (e >> 2), c = e & 3
+                    const int e = 2 * e2;
+                    const int i = 2 * h + (e >> 2);
+                    const float f0 = fmaf(scale, acc[q][e & 3][m][i], Fmt::to_f32(lo16(yo[e2])));
+                    const float f1 = fmaf(scale, acc[q][(e + 1) & 3][m][i], Fmt::to_f32(hi16(yo[e2])));
+                    o[e2] = Fmt::from_f32(f0) | (Fmt::from_f32(f1) << 16);
+                }
+                bstore16(o, yr, yoff[q][m][h]);
             }
         }
     }
@@ -785,40 +851,47 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
 
 template <class Fmt, bool kSync>
 __device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
-    const int q = (round_up_i(it.len, 16) / 16 + 3) / 4;   // column tiles per wave
     const int ms = msub_body(it.nrows);
+    const int q = expand_q(it.rank, it.nrows);
+    const int ksg = expand_ksg(it.rank, it.nrows);
     if (ms == 1) {
-        if (q <= 1) expand_body<Fmt, 1, 1, kSync>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 1, kSync>(a, it, smem);
-        else if (q <= 4) expand_body<Fmt, 4, 1, kSync>(a, it, smem);
-        else expand_body<Fmt, 8, 1, kSync>(a, it, smem);
+        if (q == 4) expand_body<Fmt, 4, 1, 1, kSync>(a, it, smem);
+        else if (q == 2) {
+            if (ksg == 1) expand_body<Fmt, 2, 1, 1, kSync>(a, it, smem);
+            else expand_body<Fmt, 2, 2, 1, kSync>(a, it, smem);
+        } else {
+            if (ksg == 2) expand_body<Fmt, 1, 2, 1, kSync>(a, it, smem);
+            else expand_body<Fmt, 1, 4, 1, kSync>(a, it, smem);
+        }
     } else if (ms == 2) {
-        if (q <= 1) expand_body<Fmt, 1, 2, kSync>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 2, kSync>(a, it, smem);
-        else if (q <= 4) expand_body<Fmt, 4, 2, kSync>(a, it, smem);
-        else expand_body<Fmt, 8, 2, kSync>(a, it, smem);
+        if (q == 2) {
+            if (ksg == 1) expand_body<Fmt, 2, 1, 2, kSync>(a, it, smem);
+            else expand_body<Fmt, 2, 2, 2, kSync>(a, it, smem);
+        } else {
+            if (ksg == 2) expand_body<Fmt, 1, 2, 2, kSync>(a, it, smem);
+            else expand_body<Fmt, 1, 4, 2, kSync>(a, it, smem);
+        }
     } else {
-        if (q <= 1) expand_body<Fmt, 1, 4, kSync>(a, it, smem);
-        else if (q <= 2) expand_body<Fmt, 2, 4, kSync>(a, it, smem);
-        else expand_body<Fmt, 4, 4, kSync>(a, it, smem);
+        if (ksg == 1) expand_body<Fmt, 1, 1, 4, kSync>(a, it, smem);
+        else if (ksg == 2) expand_body<Fmt, 1, 2, 4, kSync>(a, it, smem);
+        else expand_body<Fmt, 1, 4, 4, kSync>(a, it, smem);
     }
 }
 
 template <class Fmt>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
-lora_expand_kernel(KernelArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) lora_expand_kernel(KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLds];
-    const Item it = load_item(a.items + blockIdx.x);
+    Item it = load_item(a.items + blockIdx.x);
     if (it.kind != kItemExpand) return;
-    Item r = it;
-    resolve<kLookupAuto>(a, r);
-    expand_item<Fmt, false>(a, r, smem);
+    resolve<kLookupAuto>(a, it);
+    expand_item<Fmt, false>(a, it, smem);
 }
 
 // ---------------------------------------------------------------------------
-// Step: shrink items, then expand items, in one grid (two workgroups per CU).
-// The item list is a kernel argument of its own, ahead of the argument block,
-// so that it can be preloaded into scalar registers at wave launch.
+// Step: shrink items, then reduce items, then expand items, in one grid (two
+// workgroups per CU: the register budget is 256 per lane).  The
+// item list is a kernel argument of its own, ahead of the argument block, so
+// that it can be preloaded into scalar registers at wave launch.
 // ---------------------------------------------------------------------------
 template <class Fmt, int kLookup>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
@@ -826,34 +899,16 @@ lora_step_kernel(const DevItem* __restrict__ items, KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kStepLds];
     Item it;
     if constexpr (kLookup == kLookupArgs) {
-        const LaneTable lt = load_lane_table(a);      // in flight with the item
+        const LaneTable lt = load_lane_table();       // in flight with the item
         it = load_item(items + blockIdx.x);
-        resolve_lanes(lt, it);
+        if (it.kind != kItemReduce) resolve_lanes(lt, it);
     } else {
         it = load_item(items + blockIdx.x);
-        resolve<kLookupReg>(a, it);
+        if (it.kind != kItemReduce) resolve<kLookupReg>(a, it);
     }
     if (it.kind == kItemShrink) shrink_item<Fmt, true>(a, it, smem);
     else if (it.kind == kItemExpand) expand_item<Fmt, true>(a, it, smem);
-}
-
-// ---------------------------------------------------------------------------
-// Reduce: v(rows, 0:r) = sum of the row block's partial blocks, in order (the
-// standalone shrink's output).
-// ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kThreads) lora_reduce_kernel(KernelArgs a) {
-    const Item it = load_item(a.items + blockIdx.x);
-    if (it.kind != kItemReduce) return;
-    const int R = it.rank;
-    const int n = it.nrows * R;
-    const float* Pb = a.partials + it.part;
-    const int P = partial_parts(it.nrows, R, it.nsplit);   // the expand's order
-    for (int o = threadIdx.x; o < n; o += kThreads) {
-        float s = 0.f;
-        for (int q = 0; q < P; ++q) s += part_sum(Pb + o, it.pstride, it.nsplit, P, q);
-        const int i = o / R;
-        a.v[(int64_t)a.perm[it.p0 + i] * a.ldv + (o - i * R)] = s;
-    }
+    else if (it.kind == kItemReduce) reduce_body<true>(a, it, smem);
 }
 
 // ---------------------------------------------------------------------------
