@@ -175,9 +175,10 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.n_partials = 0;
     p.n_rb = 0;
 
-    // Prompt-sized row blocks (more than 16 rows) stream their K range in
-    // several passes; how many K ranges they are cut into follows from how
-    // many such blocks the batch has.
+    // Row blocks of more than 16 rows (prompt segments, popular adapters) are
+    // cut into about kTargetItems / (number of such blocks) K ranges: few
+    // such blocks get one pass per item (as the small blocks do), many get
+    // fewer, longer items that stream their range in several passes.
     int big_blocks = 0;
     for (int g = 0; g < p.n_groups; ++g) {
         const int r = t->host[p.group_adapter[g]].rank;
@@ -186,7 +187,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
         for (int q0 = 0; q0 < n; q0 += rb)
             if (std::min(rb, n - q0) > kInlineRows) ++big_blocks;
     }
-    const int big_split = big_blocks ? std::max(1, std::min(8, (kTargetItems + big_blocks - 1) / big_blocks)) : 1;
+    const int big_split = big_blocks ? std::max(1, (kTargetItems + big_blocks - 1) / big_blocks) : 1;
 
     for (int g = 0; g < p.n_groups; ++g) {
         const DevAdapter& ad = t->host[p.group_adapter[g]];
@@ -285,12 +286,12 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
         return fail(LORA_E_SHAPE, "batch too large: its partial results exceed 2 GiB");
 
     // device layout: [shrink items][reduce items][expand items][all reduce
-    // items][perm] |
-    // [partial and v blocks][row block counters, status] (a workspace ends
-    // here) | [step partial and v blocks x 2] (plans only: the step launch's
-    // blocks in two buffers used by alternate launches, each armed with the
-    // sentinel before the launch that reads it).  The three item lists are
-    // contiguous: the step launch runs them as one grid.
+    // items][perm] | [partial and v blocks][row block counters, status] (a
+    // workspace ends here) | [step partial and v blocks x 2] (plans only: the
+    // step launch's blocks in two buffers used by alternate launches, each
+    // armed with the sentinel before the launch that reads it).  The first
+    // three lists are contiguous: the step launch runs them as one grid; the
+    // separate launches run one each, lora_shrink the fourth.
     size_t off = 0;
     p.off_shrink = off;
     off += p.shrink.size() * sizeof(DevItem);

@@ -63,7 +63,7 @@ constexpr int kSyncStride = 32;          // 32-bit words between row block count
 constexpr int kReduceBytes = 32 * 1024;  // partial bytes one reduce item adds up at most
 constexpr int kDirectBytes = 16 * 1024;  // partial bytes up to which expand items add them up themselves
 constexpr int kMaxSplitLoads = 16;       // partial blocks one reduce thread adds up
-constexpr int kDirectSplits = 8;         // partial blocks an expand item adds up itself, at most
+constexpr int kDirectSplits = 16;        // partial blocks an expand item adds up itself, at most
 constexpr uint32_t kMaxSpan = 0x7fff0000u;  // x, y, factor and partial spans stay below 2 GiB (buffer offsets)
 static_assert(kExpandLds <= kStepLds && kReduceLds <= kStepLds, "step LDS");
 

@@ -20,11 +20,13 @@
 // Expand: one workgroup per (row block, column tile of B_g).  v is staged in
 // LDS as MFMA operand fragments holding its high and low 16-bit parts, so v
 // is never rounded to one 16-bit value.  Each wave streams B for its column
-// blocks straight into registers: a lane loads four columns of four
+// blocks straight into registers: a lane loads four columns of eight
 // consecutive ranks (8-byte loads, sixteen lanes covering a 128-byte row
-// segment) and transposes them into four operand fragments.  y^T = B^T v^T
-// runs on v_mfma_f32_16x16x16, one instruction for the high and one for the
-// low part of v.  Each lane then holds 16 columns of one row; y + s*d is
+// segment) and transposes them into four operand fragments; half-wave
+// exchanges give every lane the fragment its MFMA slot needs.  y^T = B^T v^T
+// runs on v_mfma_f32_16x16x32 whose 32 K slots hold 16 ranks twice, once with
+// the high and once with the low 16-bit part of v (the 16x16x16 form costs
+// the same per instruction on gfx950, measured, for half the work).  Each lane then holds 16 columns of one row; y + s*d is
 // rounded once to the storage dtype and written with 16-byte stores.  The B
 // tile and the y values are requested before v is read.  A row block whose
 // partial blocks are small has no reduce items: its expand items add the
@@ -66,6 +68,9 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 // Native vectors (not HIP's struct vector types): selects stay in registers.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
@@ -82,6 +87,10 @@ struct FmtF16 {
     static __device__ __forceinline__ float to_f32(uint32_t b16) {
         return (float)__builtin_bit_cast(_Float16, (uint16_t)b16);
     }
+    // two floats rounded (RNE) into one word: a low, b high
+    static __device__ __forceinline__ uint32_t pack2(float a, float b) {
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{a, b}, f16x2v));
+    }
     static __device__ __forceinline__ uint32_t from_f32(float f) {
         return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
     }
@@ -96,6 +105,9 @@ struct FmtF16 {
 };
 struct FmtBF16 {
     static __device__ __forceinline__ float to_f32(uint32_t b16) { return __uint_as_float(b16 << 16); }
+    static __device__ __forceinline__ uint32_t pack2(float a, float b) {
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{a, b}, bf16x2v));
+    }
     static __device__ __forceinline__ uint32_t from_f32(float f) {
         return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
     }
@@ -283,6 +295,14 @@ __device__ __forceinline__ bool unready4(const u32x4& v) {
     return (v.x == kSentinel) | (v.y == kSentinel) | (v.z == kSentinel) | (v.w == kSentinel);
 }
 
+// Step launch: a produced value is written with a device-coherent store and
+// read back with device-coherent loads (measured here: a plain store polled
+// through the producer's L2 is seen sooner, but a device-coherent store after
+// it costs more than that saves, and without one a consumer on another XCD
+// would depend on when the L2 writes the line back).
+__device__ __forceinline__ u32x4 sync_load16(rsrc_t r, int off) { return bload16<kCoherent>(r, off); }
+__device__ __forceinline__ void sync_store16(const u32x4& v, rsrc_t r, int off) { bstore16<kCoherent>(v, r, off); }
+
 // Step launch: wait until none of the N 16-byte values v[i] (loaded from r at
 // off[i]; masked ones read zeros) holds the sentinel, reloading those that
 // do.  budget is the thread's remaining polling rounds; once it is spent the
@@ -296,7 +316,7 @@ __device__ __forceinline__ bool any_unready(const u32x4 (&v)[N]) {
 template <int I, int N>
 __device__ __forceinline__ void reload_unready(u32x4 (&v)[N], rsrc_t r, const int (&off)[N]) {
     if constexpr (I < N) {
-        if (unready4(v[I])) v[I] = bload16<kCoherent>(r, off[I]);
+        if (unready4(v[I])) v[I] = sync_load16(r, off[I]);
         reload_unready<I + 1, N>(v, r, off);
     }
 }
@@ -343,17 +363,6 @@ __device__ __forceinline__ void transpose8x8(const u32x4 (&in)[8], u32x4 (&out)[
         out[c] = o;
     }
 }
-// The 4 x 4 transpose: in[k] holds 4 consecutive elements of row k; out[c]
-// gets element c of rows 0..3.
-__device__ __forceinline__ void transpose4x4(const u32x2 (&in)[4], u32x2 (&out)[4]) {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const int w = c >> 1;
-        out[c] = (c & 1) ? u32x2{pack_hi(in[0][w], in[1][w]), pack_hi(in[2][w], in[3][w])}
-                         : u32x2{pack_lo(in[0][w], in[1][w]), pack_lo(in[2][w], in[3][w])};
-    }
-}
-
 // ---------------------------------------------------------------------------
 // Shrink
 // ---------------------------------------------------------------------------
@@ -519,7 +528,8 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
                 const int row = m * 16 + lr;
                 const int r0 = tile * 16 + 4 * lg;
                 const bool ok = tile < NT && row < nrows && r0 < Rv;
-                bstore16<kSync ? kCoherent : 0>(as_u4(acc[m][q]), pr, ok ? (row * Rv + r0) * 4 : kOut);
+                if constexpr (kSync) sync_store16(as_u4(acc[m][q]), pr, ok ? (row * Rv + r0) * 4 : kOut);
+                else bstore16(as_u4(acc[m][q]), pr, ok ? (row * Rv + r0) * 4 : kOut);
             }
         }
     } else {
@@ -542,7 +552,8 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
             const int r0 = 4 * o - row * Rv;
             f32x4 sum = *(const f32x4*)(red + row * RS + r0);
             for (int k = 1; k < WK; ++k) sum += *(const f32x4*)(red + (k * MS * 16 + row) * RS + r0);
-            bstore16<kSync ? kCoherent : 0>(as_u4(sum), pr, 16 * o);
+            if constexpr (kSync) sync_store16(as_u4(sum), pr, 16 * o);
+            else bstore16(as_u4(sum), pr, 16 * o);
         }
     }
     if constexpr (kSync) {
@@ -613,7 +624,7 @@ __device__ __forceinline__ void reduce_body(const KernelArgs& a, const Item& it,
         for (int i = 0; i < kMaxSplitLoads; ++i) {
             const int c = q + i * G;
             off[i] = c < it.nsplit ? (c * it.pstride + it.lo + 4 * p) * 4 : kOut;
-            u[i] = bload16<kSync ? kCoherent : 0>(pr, off[i]);
+            u[i] = kSync ? sync_load16(pr, off[i]) : bload16(pr, off[i]);
         }
         if constexpr (kSync) poll16<kMaxSplitLoads>(a, u, pr, off, budget);
         f32x4 s = as_f4(u[0]);
@@ -635,7 +646,8 @@ __device__ __forceinline__ void reduce_body(const KernelArgs& a, const Item& it,
                 if (r0 + i < it.rank) dst[i] = s[i];
         } else {
             const int vo = (it.nsplit * it.pstride + f) * 4;
-            bstore16<kSync ? kCoherent : 0>(as_u4(s), pr, vo);
+            if constexpr (kSync) sync_store16(as_u4(s), pr, vo);
+            else bstore16(as_u4(s), pr, vo);
             if constexpr (kSync) {
                 // arm this slice in the other buffer for the next launch
                 const rsrc_t orr = make_rsrc(a.partials + it.part + (parity ? 0 : a.pbuf),
@@ -678,7 +690,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     const int len = it.len;
     const int nrows = it.nrows;
     const int h_out = a.h_out;
-    u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v (high | low part)
+    u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v
     const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
     const rsrc_t br = make_rsrc((const uint16_t*)it.fac + it.lo, (uint32_t)(R * h_out - it.lo) * 2);
     const float scale = it.scale;
@@ -707,42 +719,53 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
 #pragma unroll
             for (int h = 0; h < 2; ++h) yv[q][m][h] = bload16(yr, yoff[q][m][h]);
 
-    // --- B: for column block q and rank step ks, lane (lr, lg) loads rows
-    // 16ks + 4lg .. +3, columns cb*64 + base(lr) .. +3
+    // --- B.  A group is NU = Q * KSG units (column block q, rank step ks =
+    // g0 + kl); units go in pairs: lanes 0-31 load the first, lanes 32-63 the
+    // second, each lane rank octet 16ks + 8(lg & 1) (8 rows) of 4 columns
+    // cb*64 + base(lr) .. +3.  After the transpose a half-wave exchange gives
+    // every lane both units' fragments (the K slots hold each octet twice).
+    constexpr int NU = Q * KSG;
+    constexpr int NP = (NU + 1) / 2;
     const int mycol = col_base(lr);
-    u32x2 bv[Q][KSG][4];
+    u32x2 bv[NP][8];
     auto load_group = [&](int g0) __attribute__((always_inline)) {
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
+        for (int p = 0; p < NP; ++p) {
+            const int u = l < 32 ? 2 * p : (2 * p + 1 < NU ? 2 * p + 1 : 2 * p);
+            const int q = u / KSG;
+            const int kl = u - q * KSG;
             const int col = (w + 4 * q) * 64 + mycol;
+            const int j0 = 16 * (g0 + kl) + 8 * (lg & 1);
 #pragma unroll
-            for (int kl = 0; kl < KSG; ++kl)
-#pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    const int j = 16 * (g0 + kl) + 4 * lg + kk;
-                    const bool ok = j < R && col + 4 <= len;
-                    bv[q][kl][kk] = bload8(br, ok ? (j * h_out + col) * 2 : kOut);
-                }
+            for (int kk = 0; kk < 8; ++kk) {
+                const bool ok = j0 + kk < R && col + 4 <= len;
+                bv[p][kk] = bload8(br, ok ? ((j0 + kk) * h_out + col) * 2 : kOut);
+            }
         }
     };
     load_group(0);
 
-    // --- v fragments to LDS: entry (m, ks, lane) = v[row m*16 + lane%16][ranks
-    // 16ks + 4(lane/16) .. +3] as high and low 16-bit parts
+    // --- v fragments to LDS.  Entry (m, ks, lane): lanes 16g + n hold row
+    // m*16 + n, ranks 16ks + 8(g & 1) .. +7, the high part for g < 2 and the
+    // low part for g >= 2.  Task (m, ks, n, qq) fills ranks 16ks + 4qq .. +3:
+    // half (qq & 1) of lanes n + 16(qq >> 1) (high) and n + 16((qq >> 1) + 2) (low).
     {
         const bool direct = it.sub != 0;      // add the partial blocks up here
         const float* P = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
         const rsrc_t pr = make_rsrc(P, (uint32_t)(it.nsplit + 1) * it.pstride * 4);
         const int vbase = it.nsplit * it.pstride * 4;
         int budget = a.spin_limit;
+        u32x2* Vh = (u32x2*)smem;             // Vf as 8-byte halves
         const int ntask = MS * KS * 64;
         for (int task = t; task < ntask; task += kThreads) {
             const int mk = task >> 6;                 // m * KS + ks
             const int ll = task & 63;
+            const int n = ll & 15;
+            const int qq = ll >> 4;
             const int m = mk / KS;
             const int ks = mk - m * KS;
-            const int row = m * 16 + (ll & 15);
-            const int j0 = 16 * ks + 4 * (ll >> 4);
+            const int row = m * 16 + n;
+            const int j0 = 16 * ks + 4 * qq;
             const bool ok = row < nrows && j0 < R;
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
             if (a.v) {
@@ -759,7 +782,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
 #pragma unroll
                 for (int c = 0; c < kDirectSplits; ++c) {
                     off[c] = ok && c < it.nsplit ? c * it.pstride * 4 + o : kOut;
-                    u[c] = bload16<kSync ? kCoherent : 0>(pr, off[c]);
+                    u[c] = kSync ? sync_load16(pr, off[c]) : bload16(pr, off[c]);
                 }
                 if constexpr (kSync) poll16<kDirectSplits>(a, u, pr, off, budget);
                 v = as_f4(u[0]);
@@ -767,19 +790,16 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                 for (int c = 1; c < kDirectSplits; ++c) v += as_f4(u[c]);
             } else {
                 int off[1] = {ok ? vbase + (row * Rv + j0) * 4 : kOut};
-                u32x4 u[1] = {bload16<kSync ? kCoherent : 0>(pr, off[0])};
+                u32x4 u[1] = {kSync ? sync_load16(pr, off[0]) : bload16(pr, off[0])};
                 if constexpr (kSync) poll16<1>(a, u, pr, off, budget);
                 v = as_f4(u[0]);
             }
-            u32x4 f;
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const float v0 = v[2 * i], v1 = v[2 * i + 1];
-                const uint32_t h0 = Fmt::from_f32(v0), h1 = Fmt::from_f32(v1);
-                f[i] = h0 | (h1 << 16);
-                f[2 + i] = Fmt::from_f32(v0 - Fmt::to_f32(h0)) | (Fmt::from_f32(v1 - Fmt::to_f32(h1)) << 16);
-            }
-            Vf[task] = f;
+            const uint32_t h01 = Fmt::pack2(v[0], v[1]), h23 = Fmt::pack2(v[2], v[3]);
+            const uint32_t l01 = Fmt::pack2(v[0] - Fmt::to_f32(lo16(h01)), v[1] - Fmt::to_f32(hi16(h01)));
+            const uint32_t l23 = Fmt::pack2(v[2] - Fmt::to_f32(lo16(h23)), v[3] - Fmt::to_f32(hi16(h23)));
+            const int e = mk * 64 + n + 16 * (qq >> 1);
+            Vh[2 * e + (qq & 1)] = u32x2{h01, h23};
+            Vh[2 * (e + 32) + (qq & 1)] = u32x2{l01, l23};
         }
     }
     __syncthreads();
@@ -789,7 +809,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             (void)__builtin_amdgcn_atomic_inc32(a.sync + (int64_t)it.rb * kSyncStride, 2u * (uint32_t)it.nexp - 1u,
                                                 __ATOMIC_RELAXED, "agent");
 
-    // --- y^T = B^T v^T on MFMA, KSG rank steps per group
+    // --- y^T = B^T v^T on MFMA (16x16x32: 16 ranks x high and low part of v)
     f32x4 acc[Q][4][MS];
 #pragma unroll
     for (int q = 0; q < Q; ++q)
@@ -809,19 +829,35 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                 if (g0 + kl >= KS) vf[kl][m] = u32x4{0u, 0u, 0u, 0u};
             }
 #pragma unroll
-        for (int q = 0; q < Q; ++q)
+        for (int p = 0; p < NP; ++p) {
+            const int ua = 2 * p, ub = 2 * p + 1;
 #pragma unroll
-            for (int kl = 0; kl < KSG; ++kl) {
-                u32x2 fr[4];
-                transpose4x4(bv[q][kl], fr);
+            for (int c = 0; c < 4; ++c) {
+                // fragment of column c: element c of the 8 rows
+                const int wd = c >> 1;
+                u32x4 f;
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
+                for (int qq = 0; qq < 4; ++qq) {
+                    const uint32_t x0 = bv[p][2 * qq][wd], x1 = bv[p][2 * qq + 1][wd];
+                    f[qq] = (c & 1) ? pack_hi(x0, x1) : pack_lo(x0, x1);
+                }
+                u32x4 fa, fb;
 #pragma unroll
-                    for (int m = 0; m < MS; ++m) {
-                        acc[q][c][m] = Fmt::mma16(fr[c], vf[kl][m].xy, acc[q][c][m]);
-                        acc[q][c][m] = Fmt::mma16(fr[c], vf[kl][m].zw, acc[q][c][m]);
-                    }
+                for (int i = 0; i < 4; ++i) {
+                    const auto sw = __builtin_amdgcn_permlane32_swap(f[i], f[i], false, false);
+                    fa[i] = sw[0];             // lanes 0-31's unit, in every lane
+                    fb[i] = sw[1];             // lanes 32-63's unit
+                }
+#pragma unroll
+                for (int m = 0; m < MS; ++m)
+                    acc[ua / KSG][c][m] = Fmt::mma32(fa, vf[ua % KSG][m], acc[ua / KSG][c][m]);
+                if (ub < NU) {
+#pragma unroll
+                    for (int m = 0; m < MS; ++m)
+                        acc[ub / KSG][c][m] = Fmt::mma32(fb, vf[ub % KSG][m], acc[ub / KSG][c][m]);
+                }
             }
+        }
     }
 
     // --- epilogue: lane holds, for instruction c and output row 4lg + i,
@@ -841,7 +877,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                     const int i = 2 * h + (e >> 2);
                     const float f0 = fmaf(scale, acc[q][e & 3][m][i], Fmt::to_f32(lo16(yo[e2])));
                     const float f1 = fmaf(scale, acc[q][(e + 1) & 3][m][i], Fmt::to_f32(hi16(yo[e2])));
-                    o[e2] = Fmt::from_f32(f0) | (Fmt::from_f32(f1) << 16);
+                    o[e2] = Fmt::pack2(f0, f1);
                 }
                 bstore16(o, yr, yoff[q][m][h]);
             }
@@ -889,9 +925,9 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
 
 // ---------------------------------------------------------------------------
 // Step: shrink items, then reduce items, then expand items, in one grid (two
-// workgroups per CU: the register budget is 256 per lane).  The
-// item list is a kernel argument of its own, ahead of the argument block, so
-// that it can be preloaded into scalar registers at wave launch.
+// workgroups per CU: the register budget is 256 per lane).  The item list is
+// a kernel argument of its own, ahead of the argument block, so that it can
+// be preloaded into scalar registers at wave launch.
 // ---------------------------------------------------------------------------
 template <class Fmt, int kLookup>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
@@ -901,10 +937,10 @@ lora_step_kernel(const DevItem* __restrict__ items, KernelArgs a) {
     if constexpr (kLookup == kLookupArgs) {
         const LaneTable lt = load_lane_table();       // in flight with the item
         it = load_item(items + blockIdx.x);
-        if (it.kind != kItemReduce) resolve_lanes(lt, it);
+        if (it.kind == kItemShrink || it.kind == kItemExpand) resolve_lanes(lt, it);
     } else {
         it = load_item(items + blockIdx.x);
-        if (it.kind != kItemReduce) resolve<kLookupReg>(a, it);
+        if (it.kind == kItemShrink || it.kind == kItemExpand) resolve<kLookupReg>(a, it);
     }
     if (it.kind == kItemShrink) shrink_item<Fmt, true>(a, it, smem);
     else if (it.kind == kItemExpand) expand_item<Fmt, true>(a, it, smem);
