@@ -163,19 +163,24 @@ LORA_HD inline int row_block(int rank) { return round_up_i(rank, 16) > 128 ? 32 
 // in LDS, each row as sub/8 + 1 chunks of 16 bytes (an odd chunk stride: 16-
 // byte reads and writes of eight consecutive lanes hit distinct banks).
 LORA_HD inline int shrink_chunks(int sub) { return sub / 8 + 1; }
-LORA_HD inline int shrink_wn(int rank) {     // waves side by side over rank tiles: 1, 2 or 4
+// Waves side by side over rank tiles (1, 2 or 4); the others split K.  Items
+// of one 16-row subtile (decode) never split K: their MFMA work is a few
+// hundred cycles, less than adding wave sums through LDS would cost.
+LORA_HD inline int shrink_wn(int rank, int nrows) {
     const int nt = round_up_i(rank, 16) / 16;
+    if (msub_body(nrows) == 1) return 4;
     return nt >= 4 ? 4 : (nt >= 2 ? 2 : 1);
 }
-LORA_HD inline int shrink_tq(int rank) {     // rank tiles per wave: 1, 2 or 4
+LORA_HD inline int shrink_tq(int rank, int nrows) {     // rank tiles per wave: 1, 2 or 4
     const int nt = round_up_i(rank, 16) / 16;
-    const int q = (nt + shrink_wn(rank) - 1) / shrink_wn(rank);
+    const int wn = shrink_wn(rank, nrows);
+    const int q = (nt + wn - 1) / wn;
     return q <= 1 ? 1 : (q <= 2 ? 2 : 4);
 }
 LORA_HD inline int shrink_lds_bytes(int rank, int sub, int nrows) {
     const int rp = round_up_i(rank, 16);
     const int staged = (rp + msub_body(nrows) * 16) * shrink_chunks(sub) * 16;
-    const int wk = 4 / shrink_wn(rank);
+    const int wk = 4 / shrink_wn(rank, nrows);
     const int red = wk > 1 ? wk * msub_body(nrows) * 16 * (rp + 4) * 4 : 0;   // rows padded by 4 floats
     return max_i(staged, red);
 }

@@ -383,7 +383,7 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     const int KC = shrink_chunks(sub);        // 16-byte chunks per LDS row (odd)
     const int nk8 = sub / 8;
     const int nrows = it.nrows;
-    const int WN = shrink_wn(R);
+    const int WN = shrink_wn(R, nrows);
     const int WK = 4 / WN;
     const int wn = w % WN;
     const int wk = w / WN;
@@ -500,7 +500,7 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
                 for (int q = 0; q < TQ; ++q) acc[m][q] = Fmt::mma32(af[q], xf[m], acc[m][q]);
         };
         constexpr int U = TQ + MS <= 2 ? 4 : (TQ + MS <= 4 ? 2 : 1);
-        int s = wk;
+        int s = wn < NT ? wk : ks;            // a wave without a rank tile has no MFMA work
         for (; s + (U - 1) * WK < ks; s += U * WK) {
             u32x4 af[U][TQ], xf[U][MS];
 #pragma unroll
@@ -568,7 +568,7 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
 
 template <class Fmt, bool kSync>
 __device__ __forceinline__ void shrink_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
-    const int tq = shrink_tq(it.rank);
+    const int tq = shrink_tq(it.rank, it.nrows);
     const int ms = msub_body(it.nrows);
     if (tq == 1) {
         if (ms == 1) shrink_body<Fmt, 1, 1, kSync>(a, it, smem);
