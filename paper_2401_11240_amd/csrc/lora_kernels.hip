@@ -744,6 +744,31 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         }
     };
     load_group(0);
+    // MFMA operand fragments of the loaded group: column c of unit pair p, as
+    // lanes 0-31 loaded it (fa) and as lanes 32-63 loaded it (fb), in every
+    // lane.  The first group's are made right after the thread's v fill,
+    // while other threads may still wait for theirs.
+    u32x4 fa[NP][4], fb[NP][4];
+    auto prepare = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int wd = c >> 1;
+                u32x4 f;
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    const uint32_t x0 = bv[p][2 * qq][wd], x1 = bv[p][2 * qq + 1][wd];
+                    f[qq] = (c & 1) ? pack_hi(x0, x1) : pack_lo(x0, x1);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const auto sw = __builtin_amdgcn_permlane32_swap(f[i], f[i], false, false);
+                    fa[p][c][i] = sw[0];
+                    fb[p][c][i] = sw[1];
+                }
+            }
+    };
 
     // --- v fragments to LDS.  Entry (m, ks, lane): lanes 16g + n hold row
     // m*16 + n, ranks 16ks + 8(g & 1) .. +7, the high part for g < 2 and the
@@ -802,6 +827,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             Vh[2 * (e + 32) + (qq & 1)] = u32x2{l01, l23};
         }
     }
+    prepare();                                // while other threads still wait for their v
     __syncthreads();
     // step launch: this item has read its v; count it (no wait for the result)
     if constexpr (kSync)
@@ -818,7 +844,10 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
 #pragma unroll
             for (int m = 0; m < MS; ++m) acc[q][c][m] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int g0 = 0; g0 < KS; g0 += KSG) {
-        if (g0 > 0) load_group(g0);
+        if (g0 > 0) {
+            load_group(g0);
+            prepare();
+        }
         u32x4 vf[KSG][MS];
 #pragma unroll
         for (int kl = 0; kl < KSG; ++kl)
@@ -833,28 +862,13 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             const int ua = 2 * p, ub = 2 * p + 1;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-                // fragment of column c: element c of the 8 rows
-                const int wd = c >> 1;
-                u32x4 f;
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq) {
-                    const uint32_t x0 = bv[p][2 * qq][wd], x1 = bv[p][2 * qq + 1][wd];
-                    f[qq] = (c & 1) ? pack_hi(x0, x1) : pack_lo(x0, x1);
-                }
-                u32x4 fa, fb;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const auto sw = __builtin_amdgcn_permlane32_swap(f[i], f[i], false, false);
-                    fa[i] = sw[0];             // lanes 0-31's unit, in every lane
-                    fb[i] = sw[1];             // lanes 32-63's unit
-                }
 #pragma unroll
                 for (int m = 0; m < MS; ++m)
-                    acc[ua / KSG][c][m] = Fmt::mma32(fa, vf[ua % KSG][m], acc[ua / KSG][c][m]);
+                    acc[ua / KSG][c][m] = Fmt::mma32(fa[p][c], vf[ua % KSG][m], acc[ua / KSG][c][m]);
                 if (ub < NU) {
 #pragma unroll
                     for (int m = 0; m < MS; ++m)
-                        acc[ub / KSG][c][m] = Fmt::mma32(fb, vf[ub % KSG][m], acc[ub / KSG][c][m]);
+                        acc[ub / KSG][c][m] = Fmt::mma32(fb[p][c], vf[ub % KSG][m], acc[ub / KSG][c][m]);
                 }
             }
         }
