@@ -36,7 +36,10 @@
  *   - x, y, v, every A_g and B_g: 16-byte aligned device pointers;
  *   - ranks in [1, 256]; adapter indices in [-1, n_adapters);
  *   - seg_offset[0] = 0, nondecreasing, seg_offset[n_segments] = n_rows;
- *   - x and y do not overlap.
+ *   - x and y do not overlap;
+ *   - x and y each span less than 2 GiB from their first element to the end
+ *     of their last row, and h_in, h_out are at most 4 Mi (the kernels
+ *     address them with 32-bit buffer offsets).
  *
  * Asynchrony.  Every compute call is enqueued on the caller's HIP stream
  * (a hipStream_t passed as void*, NULL = the null stream) and returns
@@ -144,15 +147,18 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
  *
  * lora_plan_apply runs the whole delta (lora_apply_fused without the upload)
  * with the adapters of table t, or of the table the plan was made with when t
- * is NULL, as ONE kernel launch: its grid holds the shrink work items, then
- * the expand work items.  The float32 partial blocks of this launch live in
- * plan memory armed with a sentinel bit pattern (all ones, a NaN that no
- * 16-bit input can produce).  A shrink workgroup writes its block with
- * device-coherent stores; an expand workgroup requests its B tile and its y
- * values, then loads the partial values it needs, again while any still holds
- * the sentinel; the last expand item of a row block arms its blocks again.  A
- * workgroup waits only for workgroups earlier in the grid, which never wait,
- * and the wait is bounded: past lora_plan_set_spin_limit polling rounds per
+ * is NULL, as ONE kernel launch: its grid holds the shrink work items (float32
+ * partial results over a K range of A_g), then the reduce work items (the sum
+ * of a row block's partial results, its v), then the expand work items.  The
+ * partial and v blocks of this launch live in plan memory armed with a
+ * sentinel bit pattern (all ones, a NaN that no 16-bit input can produce);
+ * two such buffers serve alternate launches, and each producer arms its block
+ * in the other one.  Producers write with device-coherent stores; an expand
+ * workgroup requests its B tile and its y values, then loads the values it
+ * needs (v, or the partial results themselves for a row block small enough to
+ * have no reduce items), again while any still holds the sentinel.  A
+ * workgroup waits only for workgroups earlier in the grid, which never wait
+ * for later ones, and the wait is bounded: past lora_plan_set_spin_limit polling rounds per
  * thread (default 2^18, about a quarter of a second) it gives up, raises the
  * plan's status flag and finishes with invalid results, which
  * lora_plan_status reports.  The partial blocks are added in a fixed order,
@@ -164,9 +170,9 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
  * LORA_E_SHAPE / LORA_E_RANK / LORA_E_INDEX and enqueues nothing.
  *
  * lora_plan_shrink and lora_plan_expand are the two halves as separate
- * launches (one kernel each), for callers that schedule or time them apart:
- * the shrink writes the float32 partial results of x.A_g into the plan's
- * workspace, the expand adds s_g * v.B_g into y from there.  An expand must
+ * launches, for callers that schedule or time them apart: the shrink (a
+ * shrink kernel, then a reduce kernel) writes the float32 results of x.A_g
+ * into the plan's workspace, the expand adds s_g * v.B_g into y from there.  An expand must
  * follow a shrink of the same plan in stream order; the pair computes exactly
  * what lora_plan_apply computes.  Calls on one plan must be ordered (one
  * stream): they share its workspace.

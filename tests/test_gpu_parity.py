@@ -509,6 +509,11 @@ def test_errors_are_reported_not_enqueued():
         L.lora_apply_fused(p.table, L.Batch([0, 1], [99]), x, x.shape[1], y, y.shape[1], ws, n,
                            stream())
     assert e.value.code == L.LORA_E_INDEX
+    # x spanning 2 GiB or more (buffer offsets are 32-bit): refused before any launch
+    huge_ld = ((1 << 31) // (2 * max(1, w.n_rows - 1)) + 8) // 8 * 8
+    with pytest.raises(L.LoraError) as e:
+        L.lora_apply_fused(p.table, dw.batch, x, huge_ld, y, y.shape[1], ws, n, stream())
+    assert e.value.code == L.LORA_E_SHAPE
     torch.cuda.synchronize()
     assert torch.equal(y, p.y)
     dw.release()
