@@ -56,7 +56,7 @@ constexpr int kMSub = 4;                 // 16-row MFMA subtiles per item at mos
 constexpr int kInlineRows = 16;          // items this small carry their rows inline
 constexpr int kKargGroups = 128;         // groups whose pointers travel in the kernel arguments
 constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink body
-constexpr int kExpandLds = 32 * 1024;    // LDS bytes of the expand body (v fragments)
+constexpr int kExpandLds = 34 * 1024;    // LDS bytes of the expand body (v fragments, then the y tile)
 constexpr int kReduceLds = kThreads * 16;
 constexpr int kStepLds = kShrinkLds;
 constexpr int kSyncStride = 32;          // 32-bit words between row block counters (one 128-byte line each)
@@ -219,8 +219,14 @@ LORA_HD inline int expand_ksg(int rank, int nrows) {
     return ks >= cap ? cap : (ks >= 2 ? 2 : 1);
 }
 LORA_HD inline int expand_nlen(int rank, int nrows) { return 256 * expand_q(rank, nrows); }
+// v fragments; for items of more than one 16-row subtile also the y tile
+// staged through LDS afterwards ([rows][256 q / 8 + 1] chunks of 16 bytes, in
+// the same space).
 LORA_HD inline int expand_lds_bytes(int rank, int nrows) {
-    return msub_body(nrows) * (round_up_i(rank, 16) / 16) * 64 * 16;
+    const int ms = msub_body(nrows);
+    const int vf = ms * (round_up_i(rank, 16) / 16) * 64 * 16;
+    const int yt = ms > 1 ? ms * 16 * (32 * expand_q(rank, nrows) + 1) * 16 : 0;
+    return max_i(vf, yt);
 }
 
 }  // namespace lora
