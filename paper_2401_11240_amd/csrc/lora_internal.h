@@ -52,7 +52,6 @@ namespace lora {
 
 constexpr int kThreads = 256;            // workgroup size: 4 wave64
 constexpr int kMaxRank = 256;
-constexpr int kMSub = 4;                 // 16-row MFMA subtiles per item at most
 constexpr int kInlineRows = 16;          // items this small carry their rows inline
 constexpr int kKargGroups = 128;         // groups whose pointers travel in the kernel arguments
 constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink body
@@ -67,9 +66,8 @@ constexpr int kDirectSplits = 16;        // partial blocks an expand item adds u
 constexpr uint32_t kMaxSpan = 0x7fff0000u;  // x, y, factor and partial spans stay below 2 GiB (buffer offsets)
 static_assert(kExpandLds <= kStepLds && kReduceLds <= kStepLds, "step LDS");
 
-// Item kinds.
+// Item kinds (an item of any other kind does nothing).
 enum : int32_t {
-    kItemNop = 0,
     kItemShrink = 1,     // part = x(rows, k0:k0+len) . A(k0:k0+len, 0:r)
     kItemExpand = 2,     // y(rows, n0:n0+len) += s * v . B(0:r, n0:n0+len)
     kItemReduce = 3,     // v slice = sum of the row block's partial blocks

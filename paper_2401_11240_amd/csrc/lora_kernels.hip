@@ -26,11 +26,13 @@
 // exchanges give every lane the fragment its MFMA slot needs.  y^T = B^T v^T
 // runs on v_mfma_f32_16x16x32 whose 32 K slots hold 16 ranks twice, once with
 // the high and once with the low 16-bit part of v (the 16x16x16 form costs
-// the same per instruction on gfx950, measured, for half the work).  Each lane then holds 16 columns of one row; y + s*d is
-// rounded once to the storage dtype and written with 16-byte stores.  The B
-// tile and the y values are requested before v is read.  A row block whose
-// partial blocks are small has no reduce items: its expand items add the
-// partial blocks up themselves.
+// the same per instruction on gfx950, measured, for half the work).  Each
+// lane then holds 16 columns of one row; y + s*d is rounded once to the
+// storage dtype.  Items of one 16-row subtile load and store each lane's y
+// directly (16-byte accesses); larger items read and write y row by row and
+// exchange it with the MFMA layout through LDS.  The B tile and the y values
+// are requested before v is read.  A row block whose partial blocks are small
+// has no reduce items: its expand items add the partial blocks up themselves.
 //
 // Masked loads and stores are buffer operations whose offset is moved out of
 // the buffer's range: they read zeros or are dropped, with no branch.
@@ -66,8 +68,6 @@ namespace lora {
 typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
-typedef __attribute__((__vector_size__(4 * sizeof(_Float16)))) _Float16 f16x4;
-typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
 typedef float f32x2v __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
@@ -77,11 +77,9 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 // Adapter factors are reached through pointers read at run time; they are
 // global memory, said explicitly so that the loads are global, not flat.
 typedef __attribute__((address_space(1))) const uint16_t gu16;
-typedef __attribute__((address_space(1))) const u32x4 gu32x4;
-typedef __attribute__((address_space(1))) const u32x2 gu32x2;
 
 // ---------------------------------------------------------------------------
-// 16-bit storage formats and their MFMA instructions
+// 16-bit storage formats and their MFMA instruction
 // ---------------------------------------------------------------------------
 struct FmtF16 {
     static __device__ __forceinline__ float to_f32(uint32_t b16) {
@@ -91,16 +89,9 @@ struct FmtF16 {
     static __device__ __forceinline__ uint32_t pack2(float a, float b) {
         return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{a, b}, f16x2v));
     }
-    static __device__ __forceinline__ uint32_t from_f32(float f) {
-        return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
-    }
     static __device__ __forceinline__ f32x4 mma32(const u32x4& a, const u32x4& b, f32x4 c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
                                                       __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ f32x4 mma16(const u32x2& a, const u32x2& b, f32x4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a),
-                                                     __builtin_bit_cast(f16x4, b), c, 0, 0, 0);
     }
 };
 struct FmtBF16 {
@@ -108,16 +99,9 @@ struct FmtBF16 {
     static __device__ __forceinline__ uint32_t pack2(float a, float b) {
         return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{a, b}, bf16x2v));
     }
-    static __device__ __forceinline__ uint32_t from_f32(float f) {
-        return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
-    }
     static __device__ __forceinline__ f32x4 mma32(const u32x4& a, const u32x4& b, f32x4 c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                        __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ f32x4 mma16(const u32x2& a, const u32x2& b, f32x4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a),
-                                                         __builtin_bit_cast(i16x4, b), c, 0, 0, 0);
     }
 };
 
