@@ -78,6 +78,7 @@ struct DeviceGuard {
 // ---------------------------------------------------------------------------
 struct lora_table_s {
     int device = 0;
+    int n_xcd = 1;                      // XCDs of the device (workgroup p of a launch runs on XCD p % n_xcd)
     int h_in = 0, h_out = 0, dtype = 0, n = 0;
     std::vector<DevAdapter> host;
     DevAdapter* dev = nullptr;
@@ -95,10 +96,10 @@ struct HostPlan {
     int r_max = 0;
     int n_rb = 0;                       // row blocks
     std::vector<int32_t> perm, group_off, group_adapter, group_rank;
-    std::vector<DevItem> shrink, expand, reduce, reduce_all;
+    std::vector<DevItem> shrink, expand, reduce, reduce_all, step;
     int n_rows = 0;
     int64_t n_partials = 0;
-    size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_reduce_all = 0, off_perm = 0;
+    size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_reduce_all = 0, off_step = 0, off_perm = 0;
     size_t plan_bytes = 0, off_partials = 0, off_sync = 0, sync_bytes = 0, total_bytes = 0;
     size_t off_step_partials = 0, step_partials_bytes = 0, plan_total_bytes = 0;
     std::vector<unsigned char> blob;
@@ -172,6 +173,8 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.reduce.clear();
     p.reduce_all.clear();
     p.n_rows = b->n_rows;
+    p.step.clear();
+    std::vector<int64_t> rb_bytes;          // bytes each row block streams
     p.n_partials = 0;
     p.n_rb = 0;
 
@@ -210,6 +213,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
             const int ntiles = (t->h_out + nlen - 1) / nlen;
             DevItem base{};
             base.rb = p.n_rb++;
+            rb_bytes.push_back((int64_t)(r + nb) * t->h_in * 2 + (int64_t)(r + 2 * nb) * t->h_out * 2);
             base.nexp = ntiles;
             base.group = g;
             base.adapter = p.group_adapter[g];
@@ -285,13 +289,48 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     if ((uint64_t)p.n_partials * 4 > kMaxSpan)
         return fail(LORA_E_SHAPE, "batch too large: its partial results exceed 2 GiB");
 
+    // A step small enough to run in one round of workgroups (decode) gets a
+    // grid laid out per XCD: workgroup p of a launch runs on XCD p % n_xcd (the
+    // order in which the hardware hands workgroups to the XCDs), every row
+    // block gets one XCD (largest first, each to the XCD with the fewest bytes
+    // so far), and on each XCD its shrink, reduce and expand items follow in
+    // that order, slots it does not need holding items of no kind.  A row
+    // block's partial and v blocks then stay in one L2 and one fabric path.
+    // Larger steps keep the list order: there the balance of the whole grid
+    // matters more (measured: the decode step 12.9 -> 12.2 us, the 13B-layer,
+    // 70B and prompt steps 2-5% slower with the layout).  Every item still
+    // waits only on items earlier in the grid, whatever the hardware does.
+    const size_t n_step = p.shrink.size() + p.reduce.size() + p.expand.size();
+    if (t->n_xcd > 1 && n_step <= (size_t)kTargetItems) {
+        const int nx = t->n_xcd;
+        std::vector<int> home(p.n_rb, 0), order(p.n_rb);
+        for (int i = 0; i < p.n_rb; ++i) order[i] = i;
+        std::stable_sort(order.begin(), order.end(), [&](int u, int v) { return rb_bytes[u] > rb_bytes[v]; });
+        std::vector<int64_t> load(nx, 0);
+        for (int i : order) {
+            const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+            home[i] = x;
+            load[x] += rb_bytes[i];
+        }
+        std::vector<std::vector<DevItem>> q(nx);
+        for (const auto* list : {&p.shrink, &p.reduce, &p.expand})
+            for (const DevItem& it : *list) q[home[it.rb]].push_back(it);
+        size_t len = 0;
+        for (const auto& v : q) len = std::max(len, v.size());
+        const DevItem none{};                // kind 0: does nothing
+        p.step.assign(len * nx, none);
+        for (int x = 0; x < nx; ++x)
+            for (size_t i = 0; i < q[x].size(); ++i) p.step[i * nx + x] = q[x][i];
+    }
+
     // device layout: [shrink items][reduce items][expand items][all reduce
-    // items][perm] | [partial and v blocks][row block counters, status] (a
+    // items][step grid laid out per XCD, small steps only][perm] | [partial and v blocks][row block counters, status] (a
     // workspace ends here) | [step partial and v blocks x 2] (plans only: the
     // step launch's blocks in two buffers used by alternate launches, each
     // armed with the sentinel before the launch that reads it).  The first
-    // three lists are contiguous: the step launch runs them as one grid; the
-    // separate launches run one each, lora_shrink the fourth.
+    // three lists are contiguous: the step launch runs them as one grid (or the
+    // fifth, the same items laid out per XCD); the separate launches run one
+    // each, lora_shrink the fourth.
     size_t off = 0;
     p.off_shrink = off;
     off += p.shrink.size() * sizeof(DevItem);
@@ -300,7 +339,9 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.off_expand = off;
     off += p.expand.size() * sizeof(DevItem);
     p.off_reduce_all = off;
-    off = align_up(off + p.reduce_all.size() * sizeof(DevItem));
+    off += p.reduce_all.size() * sizeof(DevItem);
+    p.off_step = off;
+    off = align_up(off + p.step.size() * sizeof(DevItem));
     p.off_perm = off;
     off = align_up(off + p.perm.size() * sizeof(int32_t));
     p.plan_bytes = off;
@@ -322,6 +363,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     put(p.off_reduce, p.reduce.data(), p.reduce.size() * sizeof(DevItem));
     put(p.off_expand, p.expand.data(), p.expand.size() * sizeof(DevItem));
     put(p.off_reduce_all, p.reduce_all.data(), p.reduce_all.size() * sizeof(DevItem));
+    put(p.off_step, p.step.data(), p.step.size() * sizeof(DevItem));
     put(p.off_perm, p.perm.data(), p.perm.size() * sizeof(int32_t));
     return LORA_OK;
 }
@@ -508,8 +550,13 @@ int enqueue_step(const lora_table_s* t, const HostPlan& p, unsigned char* w, con
                  int64_t ldx, void* y, int64_t ldy, int spin_limit, hipStream_t s) {
     KernelArgs a = make_args(t, p, w, spin_limit);
     a.partials = (float*)(w + p.off_step_partials);
-    a.items = (const DevItem*)(w + p.off_shrink);
-    a.n_items = (int32_t)(p.shrink.size() + p.reduce.size() + p.expand.size());
+    if (!p.step.empty()) {                    // the grid laid out per XCD
+        a.items = (const DevItem*)(w + p.off_step);
+        a.n_items = (int32_t)p.step.size();
+    } else {
+        a.items = (const DevItem*)(w + p.off_shrink);
+        a.n_items = (int32_t)(p.shrink.size() + p.reduce.size() + p.expand.size());
+    }
     a.x = x;
     a.ldx = ldx;
     a.x_bytes = (uint32_t)span_bytes(p.n_rows, ldx, t->h_in);
@@ -585,6 +632,11 @@ int lora_register_adapters(lora_table_t* out, int device, int h_in, int h_out, i
     auto* t = new (std::nothrow) lora_table_s();
     if (!t) return fail(LORA_E_NOMEM, "table allocation failed");
     t->device = device;
+    {
+        int nx = 1;
+        if (hipDeviceGetAttribute(&nx, hipDeviceAttributeNumberOfXccs, device) != hipSuccess || nx < 1) nx = 1;
+        t->n_xcd = std::min(nx, 64);
+    }
     t->h_in = h_in;
     t->h_out = h_out;
     t->dtype = dtype;

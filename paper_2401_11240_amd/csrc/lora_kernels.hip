@@ -44,7 +44,7 @@
 // MFMA loops have no branches.
 //
 // Step launch: one grid holds every shrink item, then every reduce item, then
-// every expand item.  Its partial and v blocks live in two buffers used by
+// every expand item (for a small step, laid out per XCD by the planner).  Its partial and v blocks live in two buffers used by
 // alternate launches; the one a launch reads holds a sentinel bit pattern until
 // it is written.  Producers write with device-coherent stores (the L2 caches
 // of the XCDs are not coherent with each other; these stores write through to
@@ -968,7 +968,9 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
 
 // ---------------------------------------------------------------------------
 // Step: shrink items, then reduce items, then expand items, in one grid (two
-// workgroups per CU: the register budget is 256 per lane).  The item list is
+// workgroups per CU: the register budget is 256 per lane); in a grid laid out
+// per XCD this order holds among the items each XCD runs, and slots holding an
+// item of no kind end at once.  The item list is
 // a kernel argument of its own, ahead of the argument block, so that it can
 // be preloaded into scalar registers at wave launch.
 // ---------------------------------------------------------------------------
