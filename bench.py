@@ -42,13 +42,13 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, datasheet
 # HBM traffic of one step launch of the headline workload, from two rocprofv3
 # --pmc passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) scaled by the
 # same counters on a plain 256 MiB device copy in the same run (FETCH_SIZE
-# reads 131,088.2 KiB for 262,144 KiB read: x 1.99975; WRITE_SIZE reads
+# reads 131,092.0 KiB for 262,144 KiB read: x 1.99969; WRITE_SIZE reads
 # 262,144.0 KiB: x 1.0).  Valid only for the kernel sources it was taken on
 # (hash of csrc/*); reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "sources_sha256_16": "af784625cb3da048",
+    "sources_sha256_16": "184a69050533ee26",
     "workload": "decode_q4096_t64_mixed_rank_f16",
-    "fetch_kib": 7140.6, "fetch_scale": 262144.0 / 131088.2,
+    "fetch_kib": 6633.5, "fetch_scale": 262144.0 / 131092.0,
     "write_kib": 732.9, "write_scale": 1.0,
 }
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16
