@@ -833,6 +833,11 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         }
     }
     prepare();                                // while other threads still wait for their v
+    // decode items (one subtile) put the next rank group's B in flight from
+    // here, during the barrier and this group's MFMAs (larger items, whose B
+    // mostly comes from L2, keep the registers for their accumulators)
+    constexpr bool kAhead = MS == 1;
+    if (kAhead && KSG < KS) load_group(KSG);
     __syncthreads();
     // step launch: this item has read its v; count it (no wait for the result)
     if constexpr (kSync)
@@ -850,8 +855,9 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             for (int m = 0; m < MS; ++m) acc[q][c][m] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int g0 = 0; g0 < KS; g0 += KSG) {
         if (g0 > 0) {
-            load_group(g0);
+            if (!kAhead) load_group(g0);
             prepare();
+            if (kAhead && g0 + KSG < KS) load_group(g0 + KSG);
         }
         u32x4 vf[KSG][MS];
 #pragma unroll
