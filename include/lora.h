@@ -211,6 +211,32 @@ int lora_plan_set_spin_limit(lora_plan_t p, int32_t polls);
 int lora_group_rows(const lora_batch_t* b, int32_t n_adapters, int32_t* perm, int32_t* group_off,
                     int32_t* group_adapter, int32_t* n_groups);
 
+/*
+ * The work list a plan of this batch would run, on the host only (no GPU, no
+ * allocation): for adapters of ranks[0 .. n_adapters) on a projection
+ * h_in -> h_out, and n_xcd XCDs (the grid of a step that fits one round of
+ * workgroups is laid out per XCD; n_xcd = 1 keeps the list order).  For
+ * inspection and tests of the planner.  items[0 .. *n_items) receives every
+ * work item of the single launch in grid order (items of no kind included,
+ * kind 0), then every reduce item of lora_shrink (kind 3, grid_pos -1);
+ * capacity is the room in items.  Errors as lora_plan_create's, and
+ * LORA_E_ARG when the list does not fit (*n_items then holds the size needed).
+ */
+typedef struct {
+    int32_t kind;       /* 1 shrink, 2 expand, 3 reduce, 0 none                   */
+    int32_t row_block;  /* row block index (rows of one adapter, at most 64)      */
+    int32_t rank;
+    int32_t nrows;      /* rows of the row block                                  */
+    int32_t lo, len;    /* shrink: K range; expand: column tile; reduce: v slice  */
+    int32_t sub;        /* shrink: K per pass; expand: 1 = adds the partial blocks itself; reduce: split groups */
+    int32_t nsplit;     /* partial blocks (K ranges) of the row block             */
+    int32_t pstride;    /* floats of one partial (or v) block                     */
+    int32_t grid_pos;   /* position in the single launch's grid, -1 if not in it  */
+} lora_item_info_t;
+int lora_plan_inspect(const lora_batch_t* b, int32_t h_in, int32_t h_out, int32_t n_adapters,
+                      const int32_t* ranks, int32_t n_xcd, lora_item_info_t* items, int32_t capacity,
+                      int32_t* n_items);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* lora_last_error(void);
 

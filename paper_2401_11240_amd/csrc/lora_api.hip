@@ -298,8 +298,10 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     // block's partial and v blocks then stay in one L2 and one fabric path.
     // Larger steps keep the list order: there the balance of the whole grid
     // matters more (measured: the decode step 12.9 -> 12.2 us, the 13B-layer,
-    // 70B and prompt steps 2-5% slower with the layout).  Every item still
-    // waits only on items earlier in the grid, whatever the hardware does.
+    // 70B and prompt steps 2-5% slower with the layout), and so do steps whose
+    // row blocks cannot be spread evenly (the busiest XCD above 1.25 times the
+    // average).  Every item still waits only on items earlier in the grid,
+    // whatever the hardware does.
     const size_t n_step = p.shrink.size() + p.reduce.size() + p.expand.size();
     if (t->n_xcd > 1 && n_step <= (size_t)kTargetItems) {
         const int nx = t->n_xcd;
@@ -312,15 +314,24 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
             home[i] = x;
             load[x] += rb_bytes[i];
         }
-        std::vector<std::vector<DevItem>> q(nx);
-        for (const auto* list : {&p.shrink, &p.reduce, &p.expand})
-            for (const DevItem& it : *list) q[home[it.rb]].push_back(it);
-        size_t len = 0;
-        for (const auto& v : q) len = std::max(len, v.size());
-        const DevItem none{};                // kind 0: does nothing
-        p.step.assign(len * nx, none);
-        for (int x = 0; x < nx; ++x)
-            for (size_t i = 0; i < q[x].size(); ++i) p.step[i * nx + x] = q[x][i];
+        // only when the XCDs come out balanced: a step of few row blocks
+        // (few adapters) would otherwise leave XCDs idle
+        int64_t total = 0, most = 0;
+        for (int64_t v : load) {
+            total += v;
+            most = std::max(most, v);
+        }
+        if (4 * most * nx <= 5 * total) {
+            std::vector<std::vector<DevItem>> q(nx);
+            for (const auto* list : {&p.shrink, &p.reduce, &p.expand})
+                for (const DevItem& it : *list) q[home[it.rb]].push_back(it);
+            size_t len = 0;
+            for (const auto& v : q) len = std::max(len, v.size());
+            const DevItem none{};            // kind 0: does nothing
+            p.step.assign(len * nx, none);
+            for (int x = 0; x < nx; ++x)
+                for (size_t i = 0; i < q[x].size(); ++i) p.step[i * nx + x] = q[x][i];
+        }
     }
 
     // device layout: [shrink items][reduce items][expand items][all reduce
@@ -693,6 +704,63 @@ int lora_group_rows(const lora_batch_t* b, int32_t n_adapters, int32_t* perm, in
     std::copy(go.begin(), go.end(), group_off);
     std::copy(ga.begin(), ga.end(), group_adapter);
     *n_groups = (int32_t)ga.size();
+    return LORA_OK;
+}
+
+int lora_plan_inspect(const lora_batch_t* b, int32_t h_in, int32_t h_out, int32_t n_adapters,
+                      const int32_t* ranks, int32_t n_xcd, lora_item_info_t* items, int32_t capacity,
+                      int32_t* n_items) {
+    if (!n_items) return fail(LORA_E_ARG, "n_items is NULL");
+    *n_items = 0;
+    if (h_in <= 0 || h_out <= 0 || h_in % 8 || h_out % 8)
+        return fail(LORA_E_SHAPE, "h_in and h_out must be positive multiples of 8");
+    if ((uint64_t)std::max(h_in, h_out) * kMaxRank * 2 > kMaxSpan)
+        return fail(LORA_E_SHAPE, "h_in and h_out must be at most 4 Mi elements (factors below 2 GiB)");
+    if (n_adapters < 0 || (n_adapters > 0 && !ranks)) return fail(LORA_E_ARG, "bad adapter ranks");
+    if (capacity < 0) return fail(LORA_E_ARG, "negative capacity");
+    lora_table_s t;                           // host-side table: ranks and shapes only
+    t.h_in = h_in;
+    t.h_out = h_out;
+    t.n = n_adapters;
+    t.n_xcd = std::max(1, std::min(n_xcd, 64));
+    t.host.assign(n_adapters, DevAdapter{});
+    for (int i = 0; i < n_adapters; ++i) {
+        if (ranks[i] < 1 || ranks[i] > kMaxRank)
+            return fail(LORA_E_RANK, "adapter " + std::to_string(i) + " has rank " + std::to_string(ranks[i]) +
+                                         " outside [1, 256]");
+        t.host[i].rank = ranks[i];
+        t.host[i].scale = 1.f;
+    }
+    HostPlan p;
+    if (int rc = build_plan(&t, b, p)) return rc;
+    std::vector<const DevItem*> grid;
+    if (!p.step.empty()) {
+        for (const DevItem& it : p.step) grid.push_back(&it);
+    } else {
+        for (const auto* list : {&p.shrink, &p.reduce, &p.expand})
+            for (const DevItem& it : *list) grid.push_back(&it);
+    }
+    const size_t total = grid.size() + p.reduce_all.size();
+    if (total > (size_t)INT32_MAX) return fail(LORA_E_SHAPE, "plan too large to list");
+    *n_items = (int32_t)total;
+    if (!items) return LORA_OK;               // size query
+    if ((size_t)capacity < total) return fail(LORA_E_ARG, "capacity smaller than the plan's item count (see n_items)");
+    auto put = [&](int32_t at, const DevItem& it, int32_t pos) {
+        lora_item_info_t& o = items[at];
+        o.kind = it.kind;
+        o.row_block = it.rb;
+        o.rank = it.rank;
+        o.nrows = it.nrows;
+        o.lo = it.lo;
+        o.len = it.len;
+        o.sub = it.sub;
+        o.nsplit = it.nsplit;
+        o.pstride = it.pstride;
+        o.grid_pos = pos;
+    };
+    int32_t k = 0;
+    for (size_t i = 0; i < grid.size(); ++i, ++k) put(k, *grid[i], (int32_t)i);
+    for (const DevItem& it : p.reduce_all) put(k++, it, -1);
     return LORA_OK;
 }
 

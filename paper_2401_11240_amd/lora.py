@@ -37,7 +37,7 @@ EXPORTS = (
     "lora_register_adapters", "lora_release_adapters", "lora_workspace_bytes", "lora_shrink",
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
     "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
-    "lora_group_rows", "lora_last_error", "lora_abi_version",
+    "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
 )
 
 
@@ -106,6 +106,7 @@ def load():
         "lora_plan_status": [vp, vp],
         "lora_plan_set_spin_limit": [vp, i32],
         "lora_group_rows": [C.POINTER(_Batch), i32, i32p, i32p, i32p, i32p],
+        "lora_plan_inspect": [C.POINTER(_Batch), i32, i32, i32, i32p, i32, vp, i32, i32p],
         "lora_last_error": [],
         "lora_abi_version": [],
     }
@@ -233,3 +234,22 @@ def lora_group_rows(batch: Batch, n_adapters: int):
     _check(load().lora_group_rows(batch.c, n_adapters, p(perm), p(goff), p(gad), C.byref(G)))
     g = int(G.value)
     return perm[:int(goff[g])].copy(), goff[:g + 1].copy(), gad[:g].copy()
+
+
+# lora_item_info_t, field for field
+ITEM_INFO = np.dtype([("kind", np.int32), ("row_block", np.int32), ("rank", np.int32),
+                      ("nrows", np.int32), ("lo", np.int32), ("len", np.int32), ("sub", np.int32),
+                      ("nsplit", np.int32), ("pstride", np.int32), ("grid_pos", np.int32)])
+
+
+def lora_plan_inspect(batch: Batch, h_in: int, h_out: int, ranks: Sequence[int], n_xcd: int = 1):
+    """The work items of a plan of this batch (host only), as a structured
+    array with the fields of lora_item_info_t."""
+    r = np.ascontiguousarray(ranks, dtype=np.int32)
+    n = C.c_int32()
+    rp = r.ctypes.data_as(C.POINTER(C.c_int32))
+    _check(load().lora_plan_inspect(batch.c, h_in, h_out, len(r), rp, n_xcd, None, 0, C.byref(n)))
+    out = np.zeros(max(1, int(n.value)), dtype=ITEM_INFO)
+    _check(load().lora_plan_inspect(batch.c, h_in, h_out, len(r), rp, n_xcd, out.ctypes.data, len(out),
+                                    C.byref(n)))
+    return out[:int(n.value)]
