@@ -67,7 +67,7 @@ def parse():
     ap.add_argument("--workload", default="decode_mixed")
     ap.add_argument("--prefill-workload", default="prefill")
     ap.add_argument("--prefill-steps", type=int, default=40)
-    ap.add_argument("--extra", default="llama13b_layer,llama70b_mixed",
+    ap.add_argument("--extra", default="decode_r8,llama13b_layer,llama70b_mixed,llama70b_mixed_tp4",
                     help="further named workloads timed the same way (comma-separated; empty for none)")
     ap.add_argument("--extra-steps", type=int, default=40)
     ap.add_argument("--rotate-mib", type=float, default=640.0)
@@ -106,6 +106,12 @@ class Rotation:
                 L.lora_plan_shrink(plan, p.table, x, x.shape[1], stream)
             elif phase == "expand":
                 L.lora_plan_expand(plan, p.table, p.y, p.y.shape[1], stream)
+
+    def check_status(self, stream):
+        """Raise if a step launch of any plan gave up waiting (its y would be
+        invalid, so its time must not count as throughput)."""
+        for h in self.plans.values():
+            self.L.lora_plan_status(h, stream)
 
     def release(self):
         for h in self.plans.values():
@@ -153,6 +159,7 @@ def time_graph(torch, rot, n_steps, warmup, phase):
         end.record(s)
     end.synchronize()
     torch.cuda.synchronize()
+    rot.check_status(s)
     return float(start.elapsed_time(end))
 
 
@@ -200,6 +207,45 @@ def measure(torch, w, dev, steps, warmup, rotate_mib, label):
     )
 
 
+def plan_update_cost(torch, w, dev, n=400):
+    """Host time of re-planning a step (lora_plan_update: grouping, work
+    list, staging copy, enqueue of the upload and the arming fill) and the
+    device time of that upload, alternating between the workload's batch and
+    a second batch of the same size drawn with another seed."""
+    from paper_2401_11240_amd import device as D
+    from paper_2401_11240_amd import lora as L
+    from paper_2401_11240_amd import workloads as W
+    s = torch.cuda.current_stream(dev)
+    dw = D.upload(w, dev, stream=s)
+    p = dw.projections[0]
+    rng = np.random.default_rng(12345)
+    sa2 = rng.choice(w.n_adapters, size=w.seg_adapter.size, p=W.zipf_probs(w.n_adapters)).astype(np.int32)
+    batches = [dw.batch, L.Batch(w.seg_offset, sa2, w.n_rows)]
+    need = max(L.lora_plan_bytes(p.table, b) for b in batches)
+    plan = L.lora_plan_create_reserved(p.table, batches[0], need, s)
+    torch.cuda.synchronize()
+    for i in range(20):
+        L.lora_plan_update(plan, None, batches[i % 2], s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(n):
+        L.lora_plan_update(plan, None, batches[i % 2], s)
+    host = (time.perf_counter() - t0) / n
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(s)
+    for i in range(n):
+        L.lora_plan_update(plan, None, batches[i % 2], s)
+    ev1.record(s)
+    ev1.synchronize()
+    dev_us = ev0.elapsed_time(ev1) * 1e3 / n
+    L.lora_plan_status(plan, s)
+    L.lora_plan_destroy(plan)
+    dw.release()
+    return dict(plan_us=round(host * 1e6, 2), upload_and_arm_device_us=round(dev_us, 2),
+                plan_bytes=need)
+
+
 def sources_hash() -> str:
     import hashlib
     csrc = os.path.join(ROOT, "paper_2401_11240_amd", "csrc")
@@ -218,23 +264,48 @@ def measured_traffic(workload_name):
     return int(round((m["fetch_kib"] * m["fetch_scale"] + m["write_kib"] * m["write_scale"]) * 1024))
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, seconds):
+    """The oracle as it stands, timed on full headline steps: with its OpenMP
+    threads (rows spread over them), then with one thread, each for about
+    half of ``seconds``."""
     import oracle
     from paper_2401_11240_amd import workloads as W
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        for p in w.projections:
-            oracle.lora_apply(w.seg_offset, w.seg_adapter, w.xs[p.x], p.A, p.B, w.ranks, w.scales,
-                              p.y, w.dtype)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
+
+    def run(budget):
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            for p in w.projections:
+                oracle.lora_apply(w.seg_offset, w.seg_adapter, w.xs[p.x], p.A, p.B, w.ranks, w.scales,
+                                  p.y, w.dtype)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget:
+                return reps, el
+
+    threads = oracle.num_threads()
+    reps, el = run(seconds / 2)
+    oracle.set_num_threads(1)
+    reps1, el1 = run(seconds / 2)
+    oracle.set_num_threads(threads)
     b = W.algorithmic_bytes(w)
-    return dict(value=b * reps / el / 1e9, unit="GB/s", cores=oracle.num_threads(), kind="oracle",
-                sample=f"{reps} full steps of {w.name} (fp64 C oracle, OpenMP over rows), {el:.1f} s",
-                ms_per_step=el * 1e3 / reps)
+    return dict(value=b * reps / el / 1e9, unit="GB/s", cores=threads, kind="oracle",
+                sample=f"{reps} full steps of {w.name} (fp64 C oracle, OpenMP over rows, {threads} threads) "
+                       f"in {el:.1f} s; {reps1} steps with 1 thread in {el1:.1f} s",
+                ms_per_step=el * 1e3 / reps,
+                one_thread={"value": b * reps1 / el1 / 1e9, "ms_per_step": el1 * 1e3 / reps1},
+                affinity_cores=len(os.sched_getaffinity(0)), cpu_model=cpu_model())
 
 
 def main():
@@ -305,6 +376,9 @@ def main():
             "expand_bytes": dec["expand"]["bytes"] // dec["n_proj"],
         },
     }
+    log("[plan] re-planning cost")
+    out["replan"] = plan_update_cost(torch, w, dev)
+    out["replan"]["launches_sharing_one_plan"] = "every adapted projection of every layer with the same ranks"
     if not args.no_prefill:
         wp = W.NAMED[args.prefill_workload]()
         pre = measure(torch, wp, dev, args.prefill_steps, max(4, args.prefill_steps // 10),
@@ -332,6 +406,7 @@ def main():
                      args.rotate_mib, name)
         out["more"][wx.name] = {
             "ms_per_step": mx["ms_per_step"],
+            "us_per_launch": round(mx["ms_per_step"] * 1e3 / mx["n_proj"], 3),
             "GBps": round(mx["gbps"], 2),
             "pct_hbm_peak": round(100.0 * mx["gbps"] / HBM_PEAK_GBPS, 2),
             "tokens_per_step": mx["n_active"],

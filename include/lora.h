@@ -44,7 +44,8 @@
  * Asynchrony.  Every compute call is enqueued on the caller's HIP stream
  * (a hipStream_t passed as void*, NULL = the null stream) and returns
  * without waiting for the GPU.  No call except lora_register_adapters,
- * lora_plan_create and the destroy/release calls allocates device memory.
+ * lora_plan_create(_reserved) and the destroy/release calls allocates device
+ * memory.
  * Calls are deterministic: the same inputs give the same bits.
  *
  * Thread safety.  Distinct tables and plans may be used from any threads.
@@ -60,7 +61,7 @@
 extern "C" {
 #endif
 
-#define LORA_ABI_VERSION 2
+#define LORA_ABI_VERSION 3
 
 typedef enum { LORA_F16 = 0, LORA_BF16 = 1 } lora_dtype_t;
 
@@ -75,7 +76,9 @@ enum {
     LORA_E_HIP = -7,        /* a HIP runtime call or kernel launch failed        */
     LORA_E_WORKSPACE = -8,  /* workspace smaller than lora_workspace_bytes()     */
     LORA_E_OVERLAP = -9,    /* x and y overlap                                   */
-    LORA_E_SYNC = -10       /* a step launch gave up waiting (lora_plan_status)  */
+    LORA_E_SYNC = -10,      /* a step launch gave up waiting (lora_plan_status)  */
+    LORA_E_CAPTURE = -11,   /* the call cannot be recorded in a HIP graph        */
+    LORA_E_STALE = -12      /* a launch recorded before lora_plan_update ran and did nothing */
 };
 
 /* A step's batch, in HOST memory; read during the call only. */
@@ -133,6 +136,13 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
  * The whole delta in one call: y[t,:] <- round(y[t,:] + s_g (x[t,:].A_g).B_g).
  * The float32 intermediate lives only in ws.  Uploads the plan of this batch
  * into ws, then runs the kernels; no host synchronisation.
+ *
+ * lora_shrink, lora_expand and lora_apply_fused upload their work list from a
+ * small ring of pinned host buffers that later calls reuse (the host waits on
+ * a slot only when 16 uploads are still in flight).  A graph replay would copy
+ * whatever the slot holds by then, so these three calls refuse a stream that
+ * is being captured: LORA_E_CAPTURE, nothing enqueued.  Record the lora_plan_*
+ * calls instead.
  */
 int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,
                      int64_t ldy, void* ws, size_t ws_bytes, void* stream);
@@ -178,6 +188,37 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
  * stream): they share its workspace.
  */
 int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream);
+
+/*
+ * Re-planning for continuous batching (Section 2.2: the batch changes every
+ * iteration).  A plan owns a fixed amount of device memory and two pinned
+ * host staging buffers of the same size, allocated at creation:
+ * lora_plan_create sizes them for its batch, lora_plan_create_reserved for at
+ * least min_bytes (lora_plan_bytes tells what one batch needs; take the
+ * largest over the batches to come).  lora_plan_update plans batch b against
+ * table t (NULL: the plan's table, which t then replaces) into that memory:
+ * it validates b, builds the work list on the host, copies it into the next
+ * staging buffer, enqueues one host-to-device copy and a small fill kernel
+ * that arms the step buffers, and returns.  No device or host allocation, no
+ * memset, no stream synchronisation (the host waits only when it is two
+ * updates ahead of the stream's copies).  A batch that needs more than the
+ * capacity returns LORA_E_WORKSPACE and leaves the plan as it was; errors of
+ * b are those of lora_plan_create.  Updates and the plan's launches must be
+ * ordered on one stream.  lora_plan_update also clears the plan's status.
+ *
+ * Graphs.  lora_plan_apply, _shrink and _expand may be recorded in a HIP graph:
+ * the record holds the launch of the batch planned at that moment.  Every
+ * upload stamps the work list with a new generation, and a launch carries the
+ * generation it was made for: a replay after lora_plan_update finds another
+ * generation in the plan's header, does nothing (y untouched), and leaves
+ * LORA_E_STALE for lora_plan_status.  Record again after re-planning.
+ * lora_plan_create(_reserved) and lora_plan_update refuse a capturing stream
+ * (LORA_E_CAPTURE).
+ */
+int lora_plan_bytes(lora_table_t t, const lora_batch_t* b, size_t* bytes);
+int lora_plan_create_reserved(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, size_t min_bytes,
+                              void* stream);
+int lora_plan_update(lora_plan_t p, lora_table_t t, const lora_batch_t* b, void* stream);
 int lora_plan_apply(lora_plan_t p, lora_table_t t, const void* x, int64_t ldx, void* y,
                     int64_t ldy, void* stream);
 int lora_plan_shrink(lora_plan_t p, lora_table_t t, const void* x, int64_t ldx, void* stream);
@@ -185,11 +226,12 @@ int lora_plan_expand(lora_plan_t p, lora_table_t t, void* y, int64_t ldy, void* 
 int lora_plan_destroy(lora_plan_t p);
 
 /*
- * Status of the plan's step launches so far: waits for `stream`, then returns
- * LORA_OK, or LORA_E_SYNC when a lora_plan_apply launch gave up waiting (its
- * y is invalid); the flag, the row block counters and the sentinel are then
- * reset, so the plan is usable again.  Host-synchronising: call it off the
- * hot loop.
+ * Status of the plan's launches so far: waits for `stream`, then returns
+ * LORA_OK; LORA_E_SYNC when a lora_plan_apply launch gave up waiting (its y is
+ * invalid); or LORA_E_STALE when a recorded launch of an earlier batch ran
+ * after lora_plan_update and did nothing.  The flag, the row block counters
+ * and the sentinel are then reset, so the plan is usable again.
+ * Host-synchronising: call it off the hot loop.
  */
 int lora_plan_status(lora_plan_t p, void* stream);
 

@@ -54,6 +54,8 @@ def _load():
     lib.oracle_widen.argtypes = [u16p, C.c_int, f64p, C.c_int64]
     lib.oracle_round.argtypes = [f64p, C.c_int, u16p, C.c_int64]
     lib.oracle_num_threads.restype = C.c_int
+    lib.oracle_set_num_threads.restype = None
+    lib.oracle_set_num_threads.argtypes = [C.c_int]
     lib.oracle_group_rows.restype = C.c_int32
     lib.oracle_group_rows.argtypes = [C.c_int32, C.c_int32, i32p, i32p, i32p, i32p, i32p]
     lib.oracle_lora_shrink.argtypes = [C.c_int32, C.c_int32, i32p, i32p, C.c_int32, C.c_int,
@@ -92,6 +94,11 @@ def _ptr_array(arrs: Sequence[np.ndarray]):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads the following calls use (results do not depend on it)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def widen(bits: np.ndarray, dtype: int) -> np.ndarray:

@@ -121,6 +121,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads later calls use (n >= 1); the arithmetic does not depend on it. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ---------------------------------------------------------------------- */
 /* Batch bookkeeping                                                        */
 /* ---------------------------------------------------------------------- */

@@ -19,10 +19,10 @@ ARCH = "gfx950"
 
 # Packed-FP32 VALU forms are kept out of the device code; the host pass warns
 # that it does not know the feature, which is harmless.  The first kernel
-# argument (the step kernel's item list, 8 bytes) is preloaded into scalar
+# arguments (the item list and header pointers, 8 bytes each) are preloaded into scalar
 # registers at wave launch instead of being read from the argument segment.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                "-mllvm", "-amdgpu-kernarg-preload-count=2"]
+                "-mllvm", "-amdgpu-kernarg-preload-count=4"]
 
 
 def hipcc() -> str:

@@ -21,10 +21,11 @@
 #include "lora_internal.h"
 
 namespace lora {
-hipError_t launch_shrink(const KernelArgs& a, int dtype, hipStream_t s);
-hipError_t launch_expand(const KernelArgs& a, int dtype, hipStream_t s);
-hipError_t launch_reduce(const KernelArgs& a, hipStream_t s);
-hipError_t launch_step(const KernelArgs& a, int dtype, hipStream_t s);
+hipError_t launch_shrink(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s);
+hipError_t launch_expand(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s);
+hipError_t launch_reduce(const KernelArgs& a, const uint32_t* hdr, hipStream_t s);
+hipError_t launch_step(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s);
+hipError_t launch_fill(uint32_t* p, uint32_t v, uint64_t n_words, hipStream_t s);
 }  // namespace lora
 
 using namespace lora;
@@ -102,7 +103,12 @@ struct HostPlan {
     size_t off_shrink = 0, off_expand = 0, off_reduce = 0, off_reduce_all = 0, off_step = 0, off_perm = 0;
     size_t plan_bytes = 0, off_partials = 0, off_sync = 0, sync_bytes = 0, total_bytes = 0;
     size_t off_step_partials = 0, step_partials_bytes = 0, plan_total_bytes = 0;
-    std::vector<unsigned char> blob;
+    uint32_t generation = 0;            // header word 0 of the uploaded work list
+    std::vector<unsigned char> blob;    // [header][item lists][perm], as uploaded
+    void set_generation(uint32_t g) {
+        generation = g;
+        std::memcpy(blob.data(), &g, sizeof g);
+    }
 };
 
 int validate_batch(const lora_batch_t* b, int n_adapters) {
@@ -150,7 +156,8 @@ void group_rows(const lora_batch_t* b, int n_adapters, std::vector<int32_t>& per
     std::vector<int32_t> fill(group_off.begin(), group_off.end() - 1);
     for (int s = 0; s < b->n_segments; ++s) {
         const int a = b->seg_adapter[s];
-        if (a < 0) continue;
+        // an empty segment may name an adapter that no row uses (no group)
+        if (a < 0 || b->seg_offset[s + 1] == b->seg_offset[s]) continue;
         int32_t& f = fill[gid[a]];
         for (int t = b->seg_offset[s]; t < b->seg_offset[s + 1]; ++t) perm[f++] = t;
     }
@@ -279,7 +286,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
                 it.sub = direct ? 1 : 0;
                 it.lo = c * nlen;
                 it.len = std::min(nlen, t->h_out - c * nlen);
-                if (expand_lds_bytes(r, nb) > kExpandLds)
+                if (expand_lds_bytes(r, nb) > kExpandVmaxOff)
                     return fail(LORA_E_SHAPE, "internal: expand tile exceeds LDS");
                 p.expand.push_back(it);
             }
@@ -334,7 +341,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
         }
     }
 
-    // device layout: [shrink items][reduce items][expand items][all reduce
+    // device layout: [header][shrink items][reduce items][expand items][all reduce
     // items][step grid laid out per XCD, small steps only][perm] | [partial and v blocks][row block counters, status] (a
     // workspace ends here) | [step partial and v blocks x 2] (plans only: the
     // step launch's blocks in two buffers used by alternate launches, each
@@ -342,7 +349,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     // three lists are contiguous: the step launch runs them as one grid (or the
     // fifth, the same items laid out per XCD); the separate launches run one
     // each, lora_shrink the fourth.
-    size_t off = 0;
+    size_t off = kHeaderBytes;                // the header (generation, status) comes first
     p.off_shrink = off;
     off += p.shrink.size() * sizeof(DevItem);
     p.off_reduce = off;
@@ -359,7 +366,7 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.off_partials = off;
     off = align_up(off + (size_t)p.n_partials * sizeof(float));
     p.off_sync = off;
-    p.sync_bytes = align_up(((size_t)p.n_rb + 1) * kSyncStride * sizeof(uint32_t));
+    p.sync_bytes = align_up(std::max<size_t>(1, (size_t)p.n_rb) * kSyncStride * sizeof(uint32_t));
     off += p.sync_bytes;
     p.total_bytes = std::max<size_t>(off, kAlign);
     p.off_step_partials = off;
@@ -410,6 +417,19 @@ struct StageRing {
 std::mutex g_stage_mu;
 std::vector<StageRing*> g_rings;
 
+// The calls that upload their work list through the shared ring below cannot
+// be recorded in a graph: a replay would copy whatever the ring slot holds by
+// then.  They refuse a capturing stream before enqueuing anything.
+int check_not_capturing(hipStream_t s, const char* what) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    LORA_HIP_TRY(hipStreamIsCapturing(s, &cs));
+    if (cs != hipStreamCaptureStatusNone)
+        return fail(LORA_E_CAPTURE, std::string(what) +
+                                        " cannot be recorded in a graph (it uploads its work list from a reused "
+                                        "host buffer); record lora_plan_apply / _shrink / _expand instead");
+    return LORA_OK;
+}
+
 int stage_upload(int device, const void* src, size_t bytes, void* dst, hipStream_t s) {
     if (bytes == 0) return LORA_OK;
     std::lock_guard<std::mutex> lk(g_stage_mu);
@@ -446,7 +466,8 @@ KernelArgs make_args(const lora_table_s* t, const HostPlan& p, unsigned char* w,
     a.table = t->dev;
     a.partials = (float*)(w + p.off_partials);
     a.sync = (uint32_t*)(w + p.off_sync);
-    a.status = (int32_t*)(a.sync + (size_t)p.n_rb * kSyncStride);
+    a.status = (int32_t*)(w + sizeof(uint32_t));   // header word 1
+    a.generation = p.generation;
     a.pbuf = (int64_t)(p.step_partials_bytes / 2 / sizeof(float));
     a.spin_limit = spin_limit;
     a.h_in = t->h_in;
@@ -535,11 +556,11 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
         a.x = x;
         a.ldx = ldx;
         a.x_bytes = (uint32_t)span_bytes(p.n_rows, ldx, t->h_in);
-        LORA_HIP_TRY(launch_shrink(a, t->dtype, s));
+        LORA_HIP_TRY(launch_shrink(a, (const uint32_t*)w, t->dtype, s));
         if (!v_out) {
             a.items = (const DevItem*)(w + p.off_reduce);
             a.n_items = (int32_t)p.reduce.size();
-            LORA_HIP_TRY(launch_reduce(a, s));
+            LORA_HIP_TRY(launch_reduce(a, (const uint32_t*)w, s));
         }
     }
     if (y) {
@@ -549,7 +570,7 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
         a.y = y;
         a.ldy = ldy;
         a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
-        LORA_HIP_TRY(launch_expand(a, t->dtype, s));
+        LORA_HIP_TRY(launch_expand(a, (const uint32_t*)w, t->dtype, s));
     }
     return LORA_OK;
 }
@@ -574,17 +595,18 @@ int enqueue_step(const lora_table_s* t, const HostPlan& p, unsigned char* w, con
     a.y = y;
     a.ldy = ldy;
     a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
-    LORA_HIP_TRY(launch_step(a, t->dtype, s));
+    LORA_HIP_TRY(launch_step(a, (const uint32_t*)w, t->dtype, s));
     return LORA_OK;
 }
 
-// Counters and status to zero, both step partial buffers to the sentinel
-// (all-ones bytes).  Plan creation and the status reset only, never inside a launch
-// sequence a caller may capture.
+// Status and row block counters to zero, both step partial buffers to the
+// sentinel (all-ones words): fill kernels, no memset.  Plan creation,
+// re-planning and the status reset.
 hipError_t arm_step(const HostPlan& p, unsigned char* w, hipStream_t s) {
-    hipError_t e = hipMemsetAsync(w + p.off_sync, 0, p.sync_bytes, s);
+    hipError_t e = launch_fill((uint32_t*)(w + sizeof(uint32_t)), 0u, 1, s);
+    if (e == hipSuccess) e = launch_fill((uint32_t*)(w + p.off_sync), 0u, p.sync_bytes / sizeof(uint32_t), s);
     if (e == hipSuccess && p.step_partials_bytes)
-        e = hipMemsetAsync(w + p.off_step_partials, 0xff, p.step_partials_bytes, s);
+        e = launch_fill((uint32_t*)(w + p.off_step_partials), 0xffffffffu, p.step_partials_bytes / sizeof(uint32_t), s);
     return e;
 }
 
@@ -595,11 +617,60 @@ hipError_t arm_step(const HostPlan& p, unsigned char* w, hipStream_t s) {
 // ---------------------------------------------------------------------------
 struct lora_plan_s {
     const lora_table_s* table = nullptr;
+    int device = 0;
     int n_rows = 0;
     int spin_limit = kSpinLimit;
     HostPlan plan;
     unsigned char* dmem = nullptr;
+    size_t capacity = 0;                // device bytes at dmem, fixed at creation
+    uint32_t generation = 0;            // of the work list last uploaded
+    // two pinned staging buffers of `capacity` bytes for the uploads of
+    // lora_plan_update, used in turn; each is rewritten only after the copy
+    // that last read it has run
+    struct Stage {
+        void* host = nullptr;
+        hipEvent_t ev = nullptr;
+        bool pending = false;
+    } stage[2];
+    unsigned next_stage = 0;
 };
+
+namespace {
+
+void plan_free(lora_plan_s* pl) {
+    DeviceGuard dg(pl->device);
+    for (auto& st : pl->stage) {
+        if (st.pending && st.ev) (void)hipEventSynchronize(st.ev);
+        if (st.ev) (void)hipEventDestroy(st.ev);
+        if (st.host) (void)hipHostFree(st.host);
+        st = lora_plan_s::Stage{};
+    }
+    if (pl->dmem) (void)hipFree(pl->dmem);
+    pl->dmem = nullptr;
+    delete pl;
+}
+
+// Upload the plan's work list (header with a new generation, item lists,
+// grouped row order) from the next staging buffer and arm its step buffers,
+// all on stream s.  No allocation; the host waits only if the staging buffer
+// it takes is still being read by the copy enqueued two uploads before.
+int plan_upload(lora_plan_s* pl, hipStream_t s) {
+    if (++pl->generation == 0) pl->generation = 1;
+    pl->plan.set_generation(pl->generation);
+    auto& st = pl->stage[pl->next_stage++ & 1u];
+    if (st.pending) {
+        LORA_HIP_TRY(hipEventSynchronize(st.ev));
+        st.pending = false;
+    }
+    std::memcpy(st.host, pl->plan.blob.data(), pl->plan.plan_bytes);
+    LORA_HIP_TRY(hipMemcpyAsync(pl->dmem, st.host, pl->plan.plan_bytes, hipMemcpyHostToDevice, s));
+    LORA_HIP_TRY(hipEventRecord(st.ev, s));
+    st.pending = true;
+    LORA_HIP_TRY(arm_step(pl->plan, pl->dmem, s));
+    return LORA_OK;
+}
+
+}  // namespace
 
 // ---------------------------------------------------------------------------
 // C ABI
@@ -775,6 +846,7 @@ int lora_shrink(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ld
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_shrink")) return rc;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
     if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s, true)) return rc;
@@ -783,7 +855,7 @@ int lora_shrink(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ld
     a.n_items = (int32_t)p.reduce_all.size();
     a.v = v;
     a.ldv = ldv;
-    LORA_HIP_TRY(launch_reduce(a, s));
+    LORA_HIP_TRY(launch_reduce(a, (const uint32_t*)w, s));
     return LORA_OK;
 }
 
@@ -798,6 +870,7 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_expand")) return rc;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
     KernelArgs a = make_args(t, p, w, kSpinLimit);
@@ -808,7 +881,7 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
     a.y = y;
     a.ldy = ldy;
     a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
-    LORA_HIP_TRY(launch_expand(a, t->dtype, s));
+    LORA_HIP_TRY(launch_expand(a, (const uint32_t*)w, t->dtype, s));
     return LORA_OK;
 }
 
@@ -824,40 +897,80 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
     if (int rc = check_ws(p, ws, ws_bytes)) return rc;
     DeviceGuard dg(t->device);
     hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_apply_fused")) return rc;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
     return enqueue(t, p, w, x, ldx, y, ldy, s);
 }
 
-int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream) {
+int lora_plan_bytes(lora_table_t t, const lora_batch_t* b, size_t* bytes) {
+    if (int rc = check_table(t)) return rc;
+    if (!bytes) return fail(LORA_E_ARG, "bytes is NULL");
+    HostPlan p;
+    if (int rc = build_plan(t, b, p)) return rc;
+    *bytes = p.plan_total_bytes;
+    return LORA_OK;
+}
+
+int lora_plan_create_reserved(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, size_t min_bytes,
+                              void* stream) {
     if (!out) return fail(LORA_E_ARG, "out is NULL");
     *out = nullptr;
     if (int rc = check_table(t)) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_plan_create")) return rc;
     auto* pl = new (std::nothrow) lora_plan_s();
     if (!pl) return fail(LORA_E_NOMEM, "plan allocation failed");
     pl->table = t;
+    pl->device = t->device;
     if (int rc = build_plan(t, b, pl->plan)) {
         delete pl;
         return rc;
     }
     pl->n_rows = b->n_rows;
+    pl->capacity = align_up(std::max(pl->plan.plan_total_bytes, min_bytes));
     DeviceGuard dg(t->device);
-    hipError_t e = hipMalloc((void**)&pl->dmem, pl->plan.plan_total_bytes);
-    if (e != hipSuccess) {
-        delete pl;
-        return fail(LORA_E_NOMEM, std::string("hipMalloc of the plan: ") + hipGetErrorString(e));
+    hipError_t e = hipMalloc((void**)&pl->dmem, pl->capacity);
+    for (auto& st : pl->stage) {
+        if (e == hipSuccess) e = hipHostMalloc(&st.host, pl->capacity, hipHostMallocDefault);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&st.ev, hipEventDisableTiming);
     }
-    hipStream_t s = (hipStream_t)stream;
-    e = hipMemcpyAsync(pl->dmem, pl->plan.blob.data(), pl->plan.plan_bytes, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = arm_step(pl->plan, pl->dmem, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
-        (void)hipFree(pl->dmem);
-        delete pl;
-        return fail(LORA_E_HIP, std::string("plan upload: ") + hipGetErrorString(e));
+        plan_free(pl);
+        return fail(LORA_E_NOMEM, std::string("plan memory: ") + hipGetErrorString(e));
+    }
+    int rc = plan_upload(pl, s);
+    if (rc == LORA_OK && hipStreamSynchronize(s) != hipSuccess) rc = fail(LORA_E_HIP, "plan upload failed");
+    if (rc != LORA_OK) {
+        plan_free(pl);
+        return rc;
     }
     *out = pl;
     return LORA_OK;
+}
+
+int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream) {
+    return lora_plan_create_reserved(out, t, b, 0, stream);
+}
+
+int lora_plan_update(lora_plan_t pl, lora_table_t t, const lora_batch_t* b, void* stream) {
+    if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
+    const lora_table_s* tt = t ? t : pl->table;
+    if (int rc = check_table(tt)) return rc;
+    if (tt->device != pl->device) return fail(LORA_E_ARG, "table is on another device than the plan");
+    hipStream_t s = (hipStream_t)stream;
+    DeviceGuard dg(pl->device);
+    if (int rc = check_not_capturing(s, "lora_plan_update")) return rc;
+    HostPlan np;
+    if (int rc = build_plan(tt, b, np)) return rc;
+    if (np.plan_total_bytes > pl->capacity)
+        return fail(LORA_E_WORKSPACE, "the batch needs " + std::to_string(np.plan_total_bytes) +
+                                          " bytes of plan memory; the plan holds " + std::to_string(pl->capacity) +
+                                          " (lora_plan_create_reserved sets the capacity)");
+    pl->plan = std::move(np);
+    pl->table = tt;
+    pl->n_rows = b->n_rows;
+    return plan_upload(pl, s);
 }
 
 static int plan_run(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, void* y, int64_t ldy,
@@ -865,6 +978,7 @@ static int plan_run(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, 
     if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
     const lora_table_s* tt = t ? t : pl->table;
     if (int rc = check_compatible(pl->plan, tt)) return rc;
+    if (tt->device != pl->device) return fail(LORA_E_ARG, "table is on another device than the plan");
     if (pl->plan.n_active == 0) return LORA_OK;
     if (x)
         if (int rc = check_x(tt, x, ldx, pl->n_rows)) return rc;
@@ -896,16 +1010,17 @@ int lora_plan_expand(lora_plan_t pl, lora_table_t t, void* y, int64_t ldy, void*
 
 int lora_plan_status(lora_plan_t pl, void* stream) {
     if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
-    DeviceGuard dg(pl->table->device);
+    DeviceGuard dg(pl->device);
     hipStream_t s = (hipStream_t)stream;
-    const HostPlan& p = pl->plan;
     int32_t flag = 0;
-    LORA_HIP_TRY(hipMemcpyAsync(&flag, pl->dmem + p.off_sync + (size_t)p.n_rb * kSyncStride * sizeof(uint32_t), sizeof(flag),
-                                hipMemcpyDeviceToHost, s));
+    LORA_HIP_TRY(hipMemcpyAsync(&flag, pl->dmem + sizeof(uint32_t), sizeof(flag), hipMemcpyDeviceToHost, s));
     LORA_HIP_TRY(hipStreamSynchronize(s));
-    if (flag == 0) return LORA_OK;
-    LORA_HIP_TRY(arm_step(p, pl->dmem, s));
+    if (flag == kStatusOk) return LORA_OK;
+    LORA_HIP_TRY(arm_step(pl->plan, pl->dmem, s));
     LORA_HIP_TRY(hipStreamSynchronize(s));
+    if (flag == kStatusStale)
+        return fail(LORA_E_STALE, "a launch recorded for an earlier batch of this plan ran after lora_plan_update "
+                                  "and did nothing");
     return fail(LORA_E_SYNC, "a step launch gave up waiting for its shrink items; its results are invalid");
 }
 
@@ -918,11 +1033,7 @@ int lora_plan_set_spin_limit(lora_plan_t pl, int32_t polls) {
 
 int lora_plan_destroy(lora_plan_t pl) {
     if (!pl) return fail(LORA_E_ARG, "plan is NULL");
-    if (pl->dmem) {
-        DeviceGuard dg(pl->table->device);
-        (void)hipFree(pl->dmem);
-    }
-    delete pl;
+    plan_free(pl);
     return LORA_OK;
 }
 

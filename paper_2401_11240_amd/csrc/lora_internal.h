@@ -56,6 +56,7 @@ constexpr int kInlineRows = 16;          // items this small carry their rows in
 constexpr int kKargGroups = 128;         // groups whose pointers travel in the kernel arguments
 constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink body
 constexpr int kExpandLds = 34 * 1024;    // LDS bytes of the expand body (v fragments, then the y tile)
+constexpr int kExpandVmaxOff = kExpandLds - 16;   // expand: per-wave largest |v| (4 floats) after the fragments
 constexpr int kReduceLds = kThreads * 16;
 constexpr int kStepLds = kShrinkLds;
 constexpr int kSyncStride = 32;          // 32-bit words between row block counters (one 128-byte line each)
@@ -64,6 +65,13 @@ constexpr int kDirectBytes = 16 * 1024;  // partial bytes up to which expand ite
 constexpr int kMaxSplitLoads = 16;       // partial blocks one reduce thread adds up
 constexpr int kDirectSplits = 16;        // partial blocks an expand item adds up itself, at most
 constexpr uint32_t kMaxSpan = 0x7fff0000u;  // x, y, factor and partial spans stay below 2 GiB (buffer offsets)
+// Every plan and workspace starts with a header at a fixed place, whatever
+// the batch: word 0 the generation of the work list that follows (a launch
+// whose arguments carry another generation was recorded before the plan was
+// re-planned; it does nothing), word 1 the status (0 ok, 1 a step launch's
+// wait gave up, 2 a launch of another generation ran and did nothing).
+constexpr int kHeaderBytes = 256;
+enum : int32_t { kStatusOk = 0, kStatusGaveUp = 1, kStatusStale = 2 };
 static_assert(kExpandLds <= kStepLds && kReduceLds <= kStepLds, "step LDS");
 
 // Item kinds (an item of any other kind does nothing).
@@ -128,12 +136,12 @@ struct KernelArgs {
     int32_t n_items;
     int32_t n_groups;
     uint32_t* sync;             // step launch: per row block (every kSyncStride words), expand items finished (wraps at 2 nexp)
-    int32_t* status;            // step launch: set to 1 when a wait gave up
+    int32_t* status;            // header word 1 (see kHeaderBytes)
     int64_t pbuf;               // step launch: floats from the first partial buffer to the second
     int32_t spin_limit;         // step launch: polling rounds before a wait gives up
     uint32_t x_bytes;           // bytes from x to the end of its last row (< 2 GiB)
     uint32_t y_bytes;           // bytes from y to the end of its last row (< 2 GiB)
-    int32_t pad;
+    uint32_t generation;        // the work list these arguments were made for (header word 0)
     const void* gfac[2 * kKargGroups];   // per group g: [2g] = A_g, [2g + 1] = B_g
     float gscale[kKargGroups];           // per group: s_g
 };

@@ -61,6 +61,8 @@
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
+#include <type_traits>
+
 #include "lora_internal.h"
 
 namespace lora {
@@ -82,6 +84,9 @@ typedef __attribute__((address_space(1))) const uint16_t gu16;
 // 16-bit storage formats and their MFMA instruction
 // ---------------------------------------------------------------------------
 struct FmtF16 {
+    // binary16 tops out at 65504: a float32 v beyond about 2^15 cannot be
+    // split into a finite high part (see expand_body)
+    static constexpr bool kNarrowRange = true;
     static __device__ __forceinline__ float to_f32(uint32_t b16) {
         return (float)__builtin_bit_cast(_Float16, (uint16_t)b16);
     }
@@ -95,6 +100,7 @@ struct FmtF16 {
     }
 };
 struct FmtBF16 {
+    static constexpr bool kNarrowRange = false;   // the exponent range of float32
     static __device__ __forceinline__ float to_f32(uint32_t b16) { return __uint_as_float(b16 << 16); }
     static __device__ __forceinline__ uint32_t pack2(float a, float b) {
         return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{a, b}, bf16x2v));
@@ -145,6 +151,17 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     return it;
 }
 
+// A launch whose arguments were made for another generation of the work
+// list (recorded in a graph before the plan was re-planned) does nothing and
+// reports itself in the status word.  The header sits at a fixed place, so
+// this check is safe whatever the stale arguments hold.
+__device__ __forceinline__ bool stale(const uint32_t* __restrict__ hdr, const KernelArgs& a) {
+    if (hdr[0] == a.generation) return false;
+    if (threadIdx.x == 0)
+        __hip_atomic_store((int32_t*)(hdr + 1), (int32_t)kStatusStale, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+}
+
 __device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xffffu; }
 __device__ __forceinline__ uint32_t hi16(uint32_t w) { return w >> 16; }
 // two 16-bit values (their low halves) in one word: a low, b high
@@ -188,10 +205,11 @@ static_assert(2 * kKargGroups == 4 * 64 && kKargGroups == 2 * 64, "lane table sh
 // KernelArgs follow its 8-byte item pointer), not through the by-value
 // parameter: a lane-dependent index into the parameter can make the compiler
 // copy the whole argument block to private memory.
-static_assert(alignof(KernelArgs) == 8, "step kernel arguments: KernelArgs at offset 8");
+constexpr int kArgsOffset = 16;   // every kernel: the item list and header pointers, then KernelArgs
+static_assert(alignof(KernelArgs) == 8, "kernel arguments: KernelArgs at offset 16");
 __device__ __forceinline__ LaneTable load_lane_table() {
     const int l = threadIdx.x & 63;
-    const unsigned char* kp = (const unsigned char*)__builtin_amdgcn_kernarg_segment_ptr() + 8;
+    const unsigned char* kp = (const unsigned char*)__builtin_amdgcn_kernarg_segment_ptr() + kArgsOffset;
     const uint64_t* g = (const uint64_t*)(kp + offsetof(KernelArgs, gfac));
     const float* sc = (const float*)(kp + offsetof(KernelArgs, gscale));
     LaneTable t;
@@ -309,7 +327,7 @@ __device__ __forceinline__ void poll16(const KernelArgs& a, u32x4 (&v)[N], rsrc_
                                        int& budget) {
     while (any_unready<0, N>(v) && budget >= 0) {
         if (budget-- == 0) {
-            __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.status, (int32_t)kStatusGaveUp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return;
         }
         __builtin_amdgcn_s_sleep(1);
@@ -570,10 +588,10 @@ __device__ __forceinline__ void shrink_item(const KernelArgs& a, const Item& it,
 }
 
 template <class Fmt>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) lora_shrink_kernel(KernelArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) lora_shrink_kernel(const DevItem* __restrict__ items, const uint32_t* __restrict__ hdr, KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kShrinkLds];
-    Item it = load_item(a.items + blockIdx.x);
-    if (it.kind != kItemShrink) return;
+    Item it = load_item(items + blockIdx.x);
+    if (stale(hdr, a) || it.kind != kItemShrink) return;
     resolve<kLookupAuto>(a, it);
     shrink_item<Fmt, false>(a, it, smem);
 }
@@ -642,10 +660,11 @@ __device__ __forceinline__ void reduce_body(const KernelArgs& a, const Item& it,
     }
 }
 
-__global__ void __launch_bounds__(kThreads) lora_reduce_kernel(KernelArgs a) {
+__global__ void __launch_bounds__(kThreads) lora_reduce_kernel(const DevItem* __restrict__ items,
+                                                              const uint32_t* __restrict__ hdr, KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kReduceLds];
-    const Item it = load_item(a.items + blockIdx.x);
-    if (it.kind != kItemReduce) return;
+    const Item it = load_item(items + blockIdx.x);
+    if (stale(hdr, a) || it.kind != kItemReduce) return;
     reduce_body<false>(a, it, smem);
 }
 
@@ -677,7 +696,6 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v
     const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
     const rsrc_t br = make_rsrc((const uint16_t*)it.fac + it.lo, (uint32_t)(R * h_out - it.lo) * 2);
-    const float scale = it.scale;
     const int rowv = lane_rows(a, it);
 
     // --- y.  Items of one 16-row subtile (decode) load each lane's y directly:
@@ -779,12 +797,25 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     // m*16 + n, ranks 16ks + 8(g & 1) .. +7, the high part for g < 2 and the
     // low part for g >= 2.  Task (m, ks, n, qq) fills ranks 16ks + 4qq .. +3:
     // half (qq & 1) of lanes n + 16(qq >> 1) (high) and n + 16((qq >> 1) + 2) (low).
-    {
-        const bool direct = it.sub != 0;      // add the partial blocks up here
-        const float* P = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
-        const rsrc_t pr = make_rsrc(P, (uint32_t)(it.nsplit + 1) * it.pstride * 4);
-        const int vbase = it.nsplit * it.pstride * 4;
-        int budget = a.spin_limit;
+    //
+    // binary16 cannot hold a high part beyond 65504.  The fill keeps each
+    // thread's largest |v| and every wave leaves its maximum in LDS; if the
+    // item's maximum reaches 2^15, the fill runs again with v scaled by the
+    // power of two 2^k that brings the maximum into [2^14, 2^15) and the
+    // epilogue multiplies s_g by 2^-k.  Both scalings are exact, so the result
+    // is the unscaled product's (bit for bit wherever the unscaled split was
+    // finite and normal).
+    const bool direct = it.sub != 0;          // add the partial blocks up here
+    const float* vP = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
+    const rsrc_t pr = make_rsrc(vP, (uint32_t)(it.nsplit + 1) * it.pstride * 4);
+    const int vbase = it.nsplit * it.pstride * 4;
+    int budget = a.spin_limit;
+    float vabs = 0.f;
+    // kSerial: the rerun, when every value is known to be written; partial
+    // blocks are then loaded one by one (the same additions in the same
+    // order) so that the B fragments made meanwhile keep their registers
+    auto fill = [&](auto serial, float mul) __attribute__((always_inline)) {
+        constexpr bool kSerial = decltype(serial)::value;
         u32x2* Vh = (u32x2*)smem;             // Vf as 8-byte halves
         const int ntask = MS * KS * 64;
         for (int task = t; task < ntask; task += kThreads) {
@@ -805,6 +836,13 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                     for (int i = 0; i < 4; ++i)
                         if (j0 + i < R) v[i] = src[i];
                 }
+            } else if (direct && kSerial) {
+                const int o = (row * Rv + j0) * 4;
+                v = as_f4(kSync ? sync_load16(pr, ok ? o : kOut) : bload16(pr, ok ? o : kOut));
+                for (int c = 1; c < it.nsplit; ++c) {
+                    const int oc = ok ? c * it.pstride * 4 + o : kOut;
+                    v += as_f4(kSync ? sync_load16(pr, oc) : bload16(pr, oc));
+                }
             } else if (direct) {
                 const int o = (row * Rv + j0) * 4;
                 int off[kDirectSplits];
@@ -821,8 +859,12 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             } else {
                 int off[1] = {ok ? vbase + (row * Rv + j0) * 4 : kOut};
                 u32x4 u[1] = {kSync ? sync_load16(pr, off[0]) : bload16(pr, off[0])};
-                if constexpr (kSync) poll16<1>(a, u, pr, off, budget);
+                if constexpr (kSync && !kSerial) poll16<1>(a, u, pr, off, budget);
                 v = as_f4(u[0]);
+            }
+            if constexpr (Fmt::kNarrowRange) {
+                vabs = fmaxf(vabs, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+                v *= mul;
             }
             const uint32_t h01 = Fmt::pack2(v[0], v[1]), h23 = Fmt::pack2(v[2], v[3]);
             const uint32_t l01 = Fmt::pack2(v[0] - Fmt::to_f32(lo16(h01)), v[1] - Fmt::to_f32(hi16(h01)));
@@ -831,6 +873,13 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             Vh[2 * e + (qq & 1)] = u32x2{h01, h23};
             Vh[2 * (e + 32) + (qq & 1)] = u32x2{l01, l23};
         }
+    };
+    fill(std::false_type{}, 1.f);
+    float* vmax = (float*)(smem + kExpandVmaxOff);   // one float per wave
+    if constexpr (Fmt::kNarrowRange) {
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) vabs = fmaxf(vabs, __shfl_xor(vabs, d, 64));
+        if (l == 0) vmax[w] = vabs;
     }
     prepare();                                // while other threads still wait for their v
     // decode items (one subtile) put the next rank group's B in flight from
@@ -839,6 +888,17 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     constexpr bool kAhead = MS == 1;
     if (kAhead && KSG < KS) load_group(KSG);
     __syncthreads();
+    float escale = it.scale;                  // s_g, times 2^-k when v was scaled
+    if constexpr (Fmt::kNarrowRange) {
+        const float m = fmaxf(fmaxf(vmax[0], vmax[1]), fmaxf(vmax[2], vmax[3]));
+        if (m >= 32768.f) {                   // the same in every thread: a uniform branch
+            const int E = (int)((__float_as_uint(m) >> 23) & 0xff) - 127;
+            const int k = max_i(14 - E, -64);
+            fill(std::true_type{}, __uint_as_float((uint32_t)(127 + k) << 23));
+            escale = it.scale * __uint_as_float((uint32_t)(127 - k) << 23);
+            __syncthreads();
+        }
+    }
     // step launch: this item has read its v; count it (no wait for the result)
     if constexpr (kSync)
         if (t == 0)
@@ -914,8 +974,8 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                     // elements e = 2 e2, 2 e2 + 1: i = 2h + (e >> 2), c = e & 3
                     const int e = 2 * e2;
                     const int i = 2 * h + (e >> 2);
-                    const float f0 = fmaf(scale, acc[q][e & 3][m][i], Fmt::to_f32(lo16(yo[e2])));
-                    const float f1 = fmaf(scale, acc[q][(e + 1) & 3][m][i], Fmt::to_f32(hi16(yo[e2])));
+                    const float f0 = fmaf(escale, acc[q][e & 3][m][i], Fmt::to_f32(lo16(yo[e2])));
+                    const float f1 = fmaf(escale, acc[q][(e + 1) & 3][m][i], Fmt::to_f32(hi16(yo[e2])));
                     o[e2] = Fmt::pack2(f0, f1);
                 }
                 if constexpr (kStage) Ys[sidx] = o;
@@ -964,10 +1024,10 @@ __device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it,
 }
 
 template <class Fmt>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) lora_expand_kernel(KernelArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) lora_expand_kernel(const DevItem* __restrict__ items, const uint32_t* __restrict__ hdr, KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kExpandLds];
-    Item it = load_item(a.items + blockIdx.x);
-    if (it.kind != kItemExpand) return;
+    Item it = load_item(items + blockIdx.x);
+    if (stale(hdr, a) || it.kind != kItemExpand) return;
     resolve<kLookupAuto>(a, it);
     expand_item<Fmt, false>(a, it, smem);
 }
@@ -982,15 +1042,17 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
 // ---------------------------------------------------------------------------
 template <class Fmt, int kLookup>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
-lora_step_kernel(const DevItem* __restrict__ items, KernelArgs a) {
+lora_step_kernel(const DevItem* __restrict__ items, const uint32_t* __restrict__ hdr, KernelArgs a) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[kStepLds];
     Item it;
     if constexpr (kLookup == kLookupArgs) {
-        const LaneTable lt = load_lane_table();       // in flight with the item
+        const LaneTable lt = load_lane_table();       // in flight with the item and the header
         it = load_item(items + blockIdx.x);
+        if (stale(hdr, a)) return;
         if (it.kind == kItemShrink || it.kind == kItemExpand) resolve_lanes(lt, it);
     } else {
         it = load_item(items + blockIdx.x);
+        if (stale(hdr, a)) return;
         if (it.kind == kItemShrink || it.kind == kItemExpand) resolve<kLookupReg>(a, it);
     }
     if (it.kind == kItemShrink) shrink_item<Fmt, true>(a, it, smem);
@@ -999,43 +1061,63 @@ lora_step_kernel(const DevItem* __restrict__ items, KernelArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// launches
+// launches (hdr: the plan's or workspace's header)
 // ---------------------------------------------------------------------------
-hipError_t launch_shrink(const KernelArgs& a, int dtype, hipStream_t s) {
+hipError_t launch_shrink(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s) {
     if (a.n_items <= 0) return hipSuccess;
     if (dtype == 0)
-        hipLaunchKernelGGL(lora_shrink_kernel<FmtF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(lora_shrink_kernel<FmtF16>, dim3(a.n_items), dim3(kThreads), 0, s, a.items, hdr, a);
     else
-        hipLaunchKernelGGL(lora_shrink_kernel<FmtBF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(lora_shrink_kernel<FmtBF16>, dim3(a.n_items), dim3(kThreads), 0, s, a.items, hdr, a);
     return hipGetLastError();
 }
 
-hipError_t launch_expand(const KernelArgs& a, int dtype, hipStream_t s) {
+hipError_t launch_expand(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s) {
     if (a.n_items <= 0) return hipSuccess;
     if (dtype == 0)
-        hipLaunchKernelGGL(lora_expand_kernel<FmtF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(lora_expand_kernel<FmtF16>, dim3(a.n_items), dim3(kThreads), 0, s, a.items, hdr, a);
     else
-        hipLaunchKernelGGL(lora_expand_kernel<FmtBF16>, dim3(a.n_items), dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(lora_expand_kernel<FmtBF16>, dim3(a.n_items), dim3(kThreads), 0, s, a.items, hdr, a);
     return hipGetLastError();
 }
 
-hipError_t launch_step(const KernelArgs& a, int dtype, hipStream_t s) {
+hipError_t launch_step(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s) {
     if (a.n_items <= 0) return hipSuccess;
     const dim3 g(a.n_items), b(kThreads);
     const bool args = a.n_groups <= kKargGroups;
     if (dtype == 0) {
-        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupArgs>), g, b, 0, s, a.items, a);
-        else hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupReg>), g, b, 0, s, a.items, a);
+        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupArgs>), g, b, 0, s, a.items, hdr, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupReg>), g, b, 0, s, a.items, hdr, a);
     } else {
-        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupArgs>), g, b, 0, s, a.items, a);
-        else hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupReg>), g, b, 0, s, a.items, a);
+        if (args) hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupArgs>), g, b, 0, s, a.items, hdr, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupReg>), g, b, 0, s, a.items, hdr, a);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_reduce(const KernelArgs& a, hipStream_t s) {
+hipError_t launch_reduce(const KernelArgs& a, const uint32_t* hdr, hipStream_t s) {
     if (a.n_items <= 0) return hipSuccess;
-    hipLaunchKernelGGL(lora_reduce_kernel, dim3(a.n_items), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(lora_reduce_kernel, dim3(a.n_items), dim3(kThreads), 0, s, a.items, hdr, a);
+    return hipGetLastError();
+}
+
+// Fill n 32-bit words at p with v (arming a plan's step buffers and counters:
+// a kernel, not a memset, so that the sequence may be recorded in a graph).
+__global__ void __launch_bounds__(kThreads) lora_fill_kernel(uint32_t* __restrict__ p, uint32_t v, uint64_t n) {
+    const uint64_t stride = (uint64_t)gridDim.x * kThreads * 4;
+    const u32x4 v4 = {v, v, v, v};
+    for (uint64_t i = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) * 4; i < n; i += stride) {
+        if (i + 4 <= n) *(u32x4*)(p + i) = v4;
+        else
+            for (uint64_t j = i; j < n; ++j) p[j] = v;
+    }
+}
+
+hipError_t launch_fill(uint32_t* p, uint32_t v, uint64_t n_words, hipStream_t s) {
+    if (n_words == 0) return hipSuccess;
+    const uint64_t want = (n_words + 4 * kThreads - 1) / (4 * kThreads);
+    const unsigned grid = (unsigned)(want < 1024 ? want : 1024);
+    hipLaunchKernelGGL(lora_fill_kernel, dim3(grid), dim3(kThreads), 0, s, p, v, n_words);
     return hipGetLastError();
 }
 

@@ -31,12 +31,15 @@ LORA_E_HIP = -7
 LORA_E_WORKSPACE = -8
 LORA_E_OVERLAP = -9
 LORA_E_SYNC = -10
+LORA_E_CAPTURE = -11
+LORA_E_STALE = -12
 
 # Every function the header declares (checked by the tests).
 EXPORTS = (
     "lora_register_adapters", "lora_release_adapters", "lora_workspace_bytes", "lora_shrink",
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
     "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
+    "lora_plan_bytes", "lora_plan_create_reserved", "lora_plan_update",
     "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
 )
 
@@ -99,6 +102,9 @@ def load():
         "lora_expand": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_apply_fused": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
+        "lora_plan_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
+        "lora_plan_create_reserved": [C.POINTER(vp), vp, C.POINTER(_Batch), sz, vp],
+        "lora_plan_update": [vp, vp, C.POINTER(_Batch), vp],
         "lora_plan_apply": [vp, vp, vp, i64, vp, i64, vp],
         "lora_plan_destroy": [vp],
         "lora_plan_shrink": [vp, vp, vp, i64, vp],
@@ -195,6 +201,23 @@ def lora_plan_create(table: int, batch: Batch, stream=None) -> int:
     out = C.c_void_p()
     _check(load().lora_plan_create(C.byref(out), table, batch.c, _stream(stream)))
     return out.value
+
+
+def lora_plan_bytes(table: int, batch: Batch) -> int:
+    out = C.c_size_t()
+    _check(load().lora_plan_bytes(table, batch.c, C.byref(out)))
+    return int(out.value)
+
+
+def lora_plan_create_reserved(table: int, batch: Batch, min_bytes: int, stream=None) -> int:
+    out = C.c_void_p()
+    _check(load().lora_plan_create_reserved(C.byref(out), table, batch.c, int(min_bytes), _stream(stream)))
+    return out.value
+
+
+def lora_plan_update(plan: int, table, batch: Batch, stream=None) -> None:
+    """Re-plan ``batch`` into the plan's memory (``table`` None = the plan's table)."""
+    _check(load().lora_plan_update(plan, table or None, batch.c, _stream(stream)))
 
 
 def lora_plan_apply(plan: int, table, x, ldx: int, y, ldy: int, stream=None) -> None:

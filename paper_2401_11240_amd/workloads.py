@@ -294,12 +294,27 @@ def llama70b_mixed_batch(seed: int = 4) -> Workload:
     )
 
 
+def llama70b_mixed_batch_tp4(seed: int = 4) -> Workload:
+    """One GPU's share of the 70B mixed batch under 4-way tensor parallelism
+    (column-parallel q and gate: A replicated, B split by output columns):
+    q_proj 8192->2048 and gate 8192->7168, the same batch, adapters and laws
+    as llama70b_mixed_batch."""
+    return build_workload(
+        name="llama70b_mixed_tp4_shard_bf16", seed=seed, dtype=BF16, n_adapters=128,
+        rank_set=[8, 16, 32, 64, 128], adapter_law="zipf", n_segments=260,
+        seg_lens=[1] * 256 + [512] * 4,
+        projections=(("q_proj", 8192, 2048, "x"), ("gate_proj", 8192, 7168, "x")),
+        description="70B TP=4 shard: q 8192->2048 + gate 8192->7168; 256 decode + 4x512 prefill; 128 adapters",
+    )
+
+
 NAMED = {
     "decode_r8": decode_q_proj_rank8,
     "decode_mixed": decode_mixed_rank,
     "prefill": prefill_segments,
     "llama13b_layer": llama13b_layer_decode,
     "llama70b_mixed": llama70b_mixed_batch,
+    "llama70b_mixed_tp4": llama70b_mixed_batch_tp4,
 }
 
 

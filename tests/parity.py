@@ -9,11 +9,17 @@ Tolerance (16-bit outputs, against the oracle's unrounded double result):
     correctly rounded results.
 A stricter check rides along: against the oracle rounded once to the storage
 format, at most 1% of the elements differ at all (they may only where the
-exact value sits next to a rounding boundary and float32 accumulation lands
+exact value sits next to a rounding boundary and the kernel's arithmetic lands
 on the other side), and each that differs is the neighbouring 16-bit value or
-within one ulp plus 1e-5 times the output's RMS (float32 accumulation errors
-scale with the O(1) operands, so where y and the delta nearly cancel they are
-several ulps of the small result).
+within one ulp plus the kernel's own error bound.  That bound follows from
+its arithmetic: the expand feeds v to the MFMA as a high and a low 16-bit part
+whose sum is v to a relative 2^-16 (bfloat16: 8 + 8 significant bits; 2^-22
+for binary16), and the float32 sums over the rank and over h_in add about
+r 2^-24 and h_in 2^-24 of their terms' magnitudes.  So the delta's error is at
+most about 2^-15 times M = s_g sum_j |v_j| |B_jn| (plus the shrink's share).
+The check allows ulp(ref) + 2^-14 M (``mag``, from the oracle's v); where y and
+the delta nearly cancel that is several ulps of the small result.  Without
+``mag`` the allowance is one ulp plus 1e-5 times the output's RMS.
 """
 from __future__ import annotations
 
@@ -38,7 +44,23 @@ def bits_to_f64(bits: np.ndarray, dtype: int) -> np.ndarray:
     return W.bits_to_f32(bits, dtype).astype(np.float64)
 
 
-def compare(gpu_bits: np.ndarray, ref: np.ndarray, dtype: int, what: str = "") -> dict:
+def magnitude(w, name: str) -> np.ndarray:
+    """M[t, n] = s_g sum_j |v_tj| |B_g[j, n]| for rows with adapter g (0
+    elsewhere), v from the oracle's shrink: the scale of the terms the
+    delta's float32 sums add up."""
+    p = w.projection(name)
+    v = oracle.lora_shrink(w.seg_offset, w.seg_adapter, w.xs[p.x], p.A, w.ranks, w.dtype)
+    ra = w.row_adapter()
+    out = np.zeros((w.n_rows, p.h_out), dtype=np.float64)
+    for g in np.unique(ra[ra >= 0]):
+        rows = np.nonzero(ra == g)[0]
+        r = int(w.ranks[g])
+        b = np.abs(W.bits_to_f32(p.B[g], w.dtype).astype(np.float64)).reshape(r, p.h_out)
+        out[rows] = float(w.scales[g]) * (np.abs(v[rows, :r]) @ b)
+    return out
+
+
+def compare(gpu_bits: np.ndarray, ref: np.ndarray, dtype: int, what: str = "", mag=None) -> dict:
     gpu = bits_to_f64(gpu_bits, dtype)
     ref = np.asarray(ref, dtype=np.float64)
     assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
@@ -59,9 +81,13 @@ def compare(gpu_bits: np.ndarray, ref: np.ndarray, dtype: int, what: str = "") -
         # same sign: neighbouring patterns differ by one in the integer
         # encoding; across zero, the error itself is below one ulp
         same_sign = (gi & 0x8000) == (ri & 0x8000)
-        rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
+        if mag is None:
+            rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
+            extra = 1e-5 * rms
+        else:
+            extra = 2.0 ** -14 * np.asarray(mag, dtype=np.float64)[diff]
         ok = (same_sign & (np.abs(gi - ri) <= 1)) | (
-            np.abs(err[diff]) <= ulp(ref[diff], dtype) * 1.0001 + 1e-5 * rms)
+            np.abs(err[diff]) <= ulp(ref[diff], dtype) * 1.0001 + extra)
         one_ulp = bool(np.all(ok))
         if not one_ulp:
             idx = np.argwhere(diff)[~ok][:5]
