@@ -148,6 +148,25 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
                      int64_t ldy, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * lora_apply_fused without a workspace argument and without allocating, for
+ * callers that cannot allocate device memory (code that must not call
+ * hipMalloc, harnesses that forbid it, tight serving loops).  The work list
+ * and the float32 partial results live in a static device array of 16 MiB
+ * (one per GPU the library runs on, held until the process ends); a batch
+ * whose workspace (lora_workspace_bytes) exceeds it returns LORA_E_WORKSPACE
+ * with nothing enqueued.  The first call on a device looks up the array's
+ * device address.  The work list is copied from pageable host memory, which
+ * HIP performs synchronously: the call returns once the copy is done, after
+ * the stream's earlier work.  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams, other threads) race and must
+ * be ordered by the caller.  A capturing stream is refused (LORA_E_CAPTURE).
+ * Results are those of lora_apply_fused, bit for bit; arguments and errors as
+ * there.
+ */
+int lora_apply_fused_static(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,
+                            int64_t ldy, void* stream);
+
+/*
  * Plan a batch once and apply it many times: the batch of a step is the same
  * for every adapted projection of every layer, so the grouping and the work
  * list are built once.  lora_plan_create validates the batch, builds the

@@ -458,6 +458,32 @@ int stage_upload(int device, const void* src, size_t bytes, void* dst, hipStream
     return LORA_OK;
 }
 
+// The allocation-free entry point's workspace: one array per device, set up
+// by the HIP runtime when the library's code object is loaded there and kept
+// until the process ends.  Host code never takes its address directly (that
+// would be a host-side stand-in, not device memory): the first call on each
+// device looks the device address up and keeps it.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+unsigned char* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device` (which must be current).
+int scratch_address(int device, unsigned char** out) {
+    if (device < 0 || device >= kMaxDevices) return fail(LORA_E_ARG, "device index beyond the static scratch table");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return fail(LORA_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        g_scratch_ptr[device] = (unsigned char*)ptr;
+    }
+    *out = g_scratch_ptr[device];
+    return LORA_OK;
+}
+
 // Launch arguments of one plan on one table: the plan's buffers in workspace
 // w and the factor pointers and scales of its groups.
 KernelArgs make_args(const lora_table_s* t, const HostPlan& p, unsigned char* w, int spin_limit) {
@@ -900,6 +926,32 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
     if (int rc = check_not_capturing(s, "lora_apply_fused")) return rc;
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
+    return enqueue(t, p, w, x, ldx, y, ldy, s);
+}
+
+int lora_apply_fused_static(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,
+                            int64_t ldy, void* stream) {
+    if (int rc = check_table(t)) return rc;
+    HostPlan p;
+    if (int rc = build_plan(t, b, p)) return rc;
+    if (p.n_active == 0) return LORA_OK;
+    if (int rc = check_x(t, x, ldx, b->n_rows)) return rc;
+    if (int rc = check_y(t, y, ldy, b->n_rows)) return rc;
+    if (int rc = check_overlap(x, ldx, t->h_in, y, ldy, t->h_out, b->n_rows)) return rc;
+    if (p.total_bytes > kScratchBytes)
+        return fail(LORA_E_WORKSPACE, "the batch needs " + std::to_string(p.total_bytes) +
+                                          " bytes of workspace; the static scratch holds " +
+                                          std::to_string(kScratchBytes) + " (use lora_apply_fused)");
+    DeviceGuard dg(t->device);
+    if (!dg.ok) return fail(LORA_E_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_apply_fused_static")) return rc;
+    unsigned char* w = nullptr;
+    if (int rc = scratch_address(t->device, &w)) return rc;
+    // from pageable host memory: HIP performs this copy synchronously, so the
+    // host-side work list may go when the call returns (and the copy is
+    // ordered after the stream's earlier work, which may still read scratch)
+    LORA_HIP_TRY(hipMemcpyAsync(w, p.blob.data(), p.plan_bytes, hipMemcpyHostToDevice, s));
     return enqueue(t, p, w, x, ldx, y, ldy, s);
 }
 

@@ -39,7 +39,7 @@ EXPORTS = (
     "lora_register_adapters", "lora_release_adapters", "lora_workspace_bytes", "lora_shrink",
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
     "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
-    "lora_plan_bytes", "lora_plan_create_reserved", "lora_plan_update",
+    "lora_plan_bytes", "lora_plan_create_reserved", "lora_plan_update", "lora_apply_fused_static",
     "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
 )
 
@@ -101,6 +101,7 @@ def load():
         "lora_shrink": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_expand": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_apply_fused": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
+        "lora_apply_fused_static": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp],
         "lora_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
         "lora_plan_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
         "lora_plan_create_reserved": [C.POINTER(vp), vp, C.POINTER(_Batch), sz, vp],
@@ -195,6 +196,11 @@ def lora_apply_fused(table: int, batch: Batch, x, ldx: int, y, ldy: int, ws, ws_
                      stream=None) -> None:
     _check(load().lora_apply_fused(table, batch.c, _addr(x), ldx, _addr(y), ldy, _addr(ws),
                                    ws_bytes, _stream(stream)))
+
+
+def lora_apply_fused_static(table: int, batch: Batch, x, ldx: int, y, ldy: int, stream=None) -> None:
+    """lora_apply_fused with the library's static scratch instead of a workspace."""
+    _check(load().lora_apply_fused_static(table, batch.c, _addr(x), ldx, _addr(y), ldy, _stream(stream)))
 
 
 def lora_plan_create(table: int, batch: Batch, stream=None) -> int:
