@@ -71,6 +71,10 @@ def _load():
     lib.oracle_lora_apply_row.argtypes = [C.c_int32, C.c_int32, i32p, i32p, C.c_int32, C.c_int32,
                                           C.c_int, u16p, C.c_int64, u16pp, u16pp, i32p, f32p,
                                           u16p, C.c_int64, f64p]
+    lib.oracle_base_lora_apply.restype = C.c_int
+    lib.oracle_base_lora_apply.argtypes = [C.c_int32, C.c_int32, i32p, i32p, C.c_int32, C.c_int32,
+                                           C.c_int, u16p, C.c_int64, u16p, C.c_int64, u16pp, u16pp,
+                                           i32p, f32p, C.c_int32, f64p, C.c_int64]
     _lib = lib
     return lib
 
@@ -217,4 +221,29 @@ def lora_apply_rows(rows: Sequence[int], seg_offset, seg_adapter, x, A, B, ranks
         assert rc == 0
         out[i] = row
     del k1, k2
+    return out
+
+
+def base_lora_apply(seg_offset, seg_adapter, x, W, A, B, ranks, scales, dtype: int) -> np.ndarray:
+    """out = x . W + s_g . (x . A_g) . B_g per row, in double (unrounded); W is
+    [h_in, h_out] (the paper's H1 x H2 base weight)."""
+    so, sa = _segs(seg_offset, seg_adapter)
+    x = _c16(x)
+    W = _c16(W)
+    T, h_in = x.shape
+    assert W.shape[0] == h_in, (W.shape, h_in)
+    h_out = W.shape[1]
+    ranks = np.ascontiguousarray(ranks, dtype=np.int32)
+    scales = np.ascontiguousarray(scales, dtype=np.float32)
+    out = np.empty((T, h_out), dtype=np.float64)
+    Ap, k1 = _ptr_array(A)
+    Bp, k2 = _ptr_array(B)
+    r_max = int(ranks.max()) if ranks.size else 1
+    rc = _load().oracle_base_lora_apply(T, sa.shape[0], _ptr(so, C.c_int32), _ptr(sa, C.c_int32), h_in,
+                                        h_out, dtype, _ptr(x, C.c_uint16), h_in, _ptr(W, C.c_uint16), h_out,
+                                        Ap, Bp, _ptr(ranks, C.c_int32), _ptr(scales, C.c_float), r_max,
+                                        _ptr(out, C.c_double), h_out)
+    del k1, k2
+    if rc != 0:
+        raise MemoryError("oracle_base_lora_apply")
     return out

@@ -254,6 +254,45 @@ int oracle_lora_apply(int32_t n_rows, int32_t n_segments, const int32_t* seg_off
     return 0;
 }
 
+/* Eq. 1 whole (Section 2.1): y' = xW + xAB, the base projection and the
+ * adapter delta together, with the per-adapter scale:
+ *     out[t, n] = sum_k x[t,k] W[k,n]  +  s_g sum_j v[t,j] B_g[j,n],
+ *     v[t, j]   = sum_k x[t,k] A_g[k,j]
+ * W is the paper's H1 x H2 weight, [h_in, h_out] row-major with leading
+ * dimension ldw.  Rows with adapter -1 get x.W alone.  Double, k and j
+ * ascending, the base sum and the delta added once at the end. */
+int oracle_base_lora_apply(int32_t n_rows, int32_t n_segments, const int32_t* seg_offset,
+                           const int32_t* seg_adapter, int32_t h_in, int32_t h_out, int dtype,
+                           const uint16_t* x, int64_t ldx, const uint16_t* W, int64_t ldw,
+                           const uint16_t* const* A, const uint16_t* const* B, const int32_t* ranks,
+                           const float* scales, int32_t r_max, double* out, int64_t ldo) {
+    int64_t ldv = r_max > 0 ? r_max : 1;
+    double* v = (double*)calloc((size_t)(n_rows > 0 ? n_rows : 1) * (size_t)ldv, sizeof(double));
+    if (!v) return -1;
+    oracle_lora_shrink(n_rows, n_segments, seg_offset, seg_adapter, h_in, dtype, x, ldx, A, ranks,
+                       v, ldv);
+    int32_t t;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (t = 0; t < n_rows; ++t) {
+        const int32_t g = row_adapter(t, n_segments, seg_offset, seg_adapter);
+        for (int32_t n = 0; n < h_out; ++n) {
+            double base = 0.0;
+            for (int32_t k = 0; k < h_in; ++k)
+                base += widen(x[(int64_t)t * ldx + k], dtype) * widen(W[(int64_t)k * ldw + n], dtype);
+            double delta = 0.0;
+            if (g >= 0) {
+                double acc = 0.0;
+                for (int32_t j = 0; j < ranks[g]; ++j)
+                    acc += v[(int64_t)t * ldv + j] * widen(B[g][(int64_t)j * h_out + n], dtype);
+                delta = (double)scales[g] * acc;
+            }
+            out[(int64_t)t * ldo + n] = base + delta;
+        }
+    }
+    free(v);
+    return 0;
+}
+
 /* One output row only (for sampled checks at full size): out[0..h_out). */
 int oracle_lora_apply_row(int32_t t, int32_t n_segments, const int32_t* seg_offset,
                           const int32_t* seg_adapter, int32_t h_in, int32_t h_out, int dtype,

@@ -19,7 +19,9 @@ Draw order, for one ``numpy.random.default_rng(seed)``:
   2. adapter index per segment, then segment lengths,
   3. every distinct input tensor ``x``,
   4. for each projection, for each adapter: ``A`` then ``B``,
-  5. for each projection: the base output ``y``.
+  5. for each projection: the base output ``y``,
+  6. only for workloads of the fused base projection: for each projection,
+     the base weight ``W`` [h_in, h_out] (the paper's H1 x H2 weight).
 """
 from __future__ import annotations
 
@@ -91,6 +93,7 @@ class Projection:
     A: List[np.ndarray]         # per adapter, uint16 [h_in, r_g], row-major
     B: List[np.ndarray]         # per adapter, uint16 [r_g, h_out], row-major
     y: np.ndarray               # uint16 [n_rows, h_out], the base output x.W
+    W: Optional[np.ndarray] = None   # uint16 [h_in, h_out]: the base weight (fused base workloads only)
 
 
 @dataclass
@@ -143,6 +146,7 @@ def build_workload(
     xs: Optional[Dict[str, int]] = None,
     scale: Optional[float] = None,
     description: str = "",
+    base_weight: bool = False,
 ) -> Workload:
     """Draw one workload in the fixed draw order.
 
@@ -213,6 +217,11 @@ def build_workload(
     # 5. base outputs
     for p in projs:
         p.y = normal_bits(rng, (n_rows, p.h_out), 1.0, dtype)
+
+    # 6. base weights, W ~ N(0, 1/h_in) so that x.W ~ N(0, 1)
+    if base_weight:
+        for p in projs:
+            p.W = normal_bits(rng, (p.h_in, p.h_out), 1.0 / np.sqrt(p.h_in), dtype)
 
     return Workload(
         name=name, dtype=dtype, n_rows=n_rows, seg_offset=seg_offset, seg_adapter=sa,
@@ -306,6 +315,35 @@ def llama70b_mixed_batch_tp4(seed: int = 4) -> Workload:
         projections=(("q_proj", 8192, 2048, "x"), ("gate_proj", 8192, 7168, "x")),
         description="70B TP=4 shard: q 8192->2048 + gate 8192->7168; 256 decode + 4x512 prefill; 128 adapters",
     )
+
+
+def prefill_base(seed: int = 2) -> Workload:
+    """The prompt workload (16 segments, len U[64,1024], one adapter each, r in
+    {8..64}, 4096->4096, bf16) with the base weight W of the projection: the
+    whole of Eq. 1, y' = xW + s(xA)B, for the fused base projection."""
+    return build_workload(
+        name="prefill_base_q4096_16seg_bf16", seed=seed, dtype=BF16, n_adapters=16,
+        rank_set=[8, 16, 32, 64], adapter_law="identity", n_segments=16,
+        len_range=(64, 1024), projections=(("q_proj", 4096, 4096, "x"),), base_weight=True,
+        description="prefill 16 segments + base weight: y = xW + s(xA)B, 4096->4096, bf16",
+    )
+
+
+def prefill_base_one_segment(seed: int = 5) -> Workload:
+    """One prompt of 1024 tokens with one rank-64 adapter, 4096->4096, bf16,
+    with the base weight: the single-prompt shape of the fused base projection."""
+    return build_workload(
+        name="prefill_base_l1024_r64_bf16", seed=seed, dtype=BF16, n_adapters=1,
+        fixed_ranks=[64], seg_adapter=[0], seg_lens=[1024],
+        projections=(("q_proj", 4096, 4096, "x"),), base_weight=True,
+        description="one 1024-token prompt, rank 64, + base weight, 4096->4096, bf16",
+    )
+
+
+BASE_NAMED = {
+    "prefill_base": prefill_base,
+    "prefill_base_l1024": prefill_base_one_segment,
+}
 
 
 NAMED = {

@@ -415,3 +415,95 @@ def test_algorithmic_bytes_counts_distinct_adapters_once():
     exp = 2 * ((8 + 16) * (32 + 64) + 4 * 32 + 4 * 2 * 64)
     assert W.algorithmic_bytes(w) == exp
     assert W.algorithmic_flops(w) == 2 * (8 * 3 + 16) * (32 + 64)
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1 whole: the base projection with the delta (oracle.base_lora_apply)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", [W.F16, W.BF16])
+@pytest.mark.parametrize("seed", range(4))
+def test_base_lora_exact_integers_vs_merged_weight(dtype, seed):
+    """x.W + s.(x.A).B equals x.(W + s.A.B) (Eq. 1, the merged weight W') in
+    exact integer arithmetic; W is not square, so a transposed W fails."""
+    rng = np.random.default_rng(300 + seed)
+    h_in, h_out, n_ad = 6, 5, 3
+    ranks = [2, 1, 4]
+    T = 8
+    sa = rng.integers(-1, n_ad, T).astype(np.int32)
+    so = np.arange(T + 1, dtype=np.int32)
+    xi = _small_ints(rng, (T, h_in))
+    Wi = _small_ints(rng, (h_in, h_out), -6, 7)
+    Ai = [_small_ints(rng, (h_in, r)) for r in ranks]
+    Bi = [_small_ints(rng, (r, h_out)) for r in ranks]
+    scales = np.array([0.5, 4.0, 0.125], dtype=np.float32)
+    to = lambda a: _bits(a, dtype)
+    out = oracle.base_lora_apply(so, sa, to(xi), to(Wi), [to(a) for a in Ai], [to(b) for b in Bi], ranks,
+                                 scales, dtype)
+    assert out.shape == (T, h_out)
+    for t in range(T):
+        g = int(sa[t])
+        for n in range(h_out):
+            merged = [Fraction(int(Wi[k, n])) for k in range(h_in)]
+            if g >= 0:
+                for k in range(h_in):
+                    merged[k] += Fraction(float(scales[g])) * sum(int(Ai[g][k, j]) * int(Bi[g][j, n])
+                                                                  for j in range(ranks[g]))
+            exact = sum(int(xi[t, k]) * merged[k] for k in range(h_in))
+            assert Fraction(out[t, n]) == exact, (t, n)
+
+
+def test_base_lora_without_adapters_is_blas_matmul():
+    """Rows with adapter -1 get x.W alone: numpy's BLAS product of the widened
+    inputs (another implementation) agrees to double rounding."""
+    rng = np.random.default_rng(21)
+    dtype = W.BF16
+    h_in, h_out, T = 96, 40, 11
+    x = W.normal_bits(rng, (T, h_in), 1.0, dtype)
+    Wb = W.normal_bits(rng, (h_in, h_out), 1 / np.sqrt(h_in), dtype)
+    A = W.normal_bits(rng, (h_in, 8), 0.1, dtype)
+    B = W.normal_bits(rng, (8, h_out), 0.1, dtype)
+    out = oracle.base_lora_apply([0, T], [-1], x, Wb, [A], [B], [8], [1.0], dtype)
+    ref = oracle.widen(x, dtype) @ oracle.widen(Wb, dtype)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-13)
+
+
+def test_base_lora_with_zero_weight_is_the_delta():
+    """W = 0 leaves s.(x.A).B: the delta oracle on a zero base output."""
+    rng = np.random.default_rng(22)
+    dtype = W.F16
+    h_in, h_out, T = 48, 24, 6
+    x = W.normal_bits(rng, (T, h_in), 1.0, dtype)
+    ranks = [3, 8]
+    A = [W.normal_bits(rng, (h_in, r), 0.2, dtype) for r in ranks]
+    B = [W.normal_bits(rng, (r, h_out), 0.2, dtype) for r in ranks]
+    so, sa = [0, 2, 3, 6], [1, -1, 0]
+    out = oracle.base_lora_apply(so, sa, x, np.zeros((h_in, h_out), np.uint16), A, B, ranks, [2.0, 0.5], dtype)
+    ref = oracle.lora_apply(so, sa, x, A, B, ranks, [2.0, 0.5], np.zeros((T, h_out), np.uint16), dtype)
+    assert np.array_equal(out, ref)
+
+
+def test_base_lora_brute_force_tiny():
+    """Pure-Python loops of Eq. 1 on tiny shapes, in the order y' = xW + s(xA)B."""
+    rng = np.random.default_rng(23)
+    dtype = W.BF16
+    h_in, h_out, T = 5, 7, 4
+    ranks = [2, 3]
+    x = W.normal_bits(rng, (T, h_in), 1.0, dtype)
+    Wb = W.normal_bits(rng, (h_in, h_out), 0.5, dtype)
+    A = [W.normal_bits(rng, (h_in, r), 0.5, dtype) for r in ranks]
+    B = [W.normal_bits(rng, (r, h_out), 0.5, dtype) for r in ranks]
+    so, sa, scales = [0, 1, 3, 4], [1, 0, -1], [0.75, 1.5]
+    out = oracle.base_lora_apply(so, sa, x, Wb, A, B, ranks, scales, dtype)
+    xf, Wf = oracle.widen(x, dtype), oracle.widen(Wb, dtype)
+    row_ad = [1, 0, 0, -1]
+    for t in range(T):
+        g = row_ad[t]
+        for n in range(h_out):
+            base = sum(float(xf[t, k]) * float(Wf[k, n]) for k in range(h_in))
+            d = 0.0
+            if g >= 0:
+                Af, Bf = oracle.widen(A[g], dtype), oracle.widen(B[g], dtype)
+                v = [sum(float(xf[t, k]) * float(Af[k, j]) for k in range(h_in)) for j in range(ranks[g])]
+                d = scales[g] * sum(v[j] * float(Bf[j, n]) for j in range(ranks[g]))
+            assert abs(out[t, n] - (base + d)) <= 1e-12 * (1 + abs(base + d)), (t, n)
