@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--extra", default="decode_r8,llama13b_layer,llama70b_mixed,llama70b_mixed_tp4",
                     help="further named workloads timed the same way (comma-separated; empty for none)")
     ap.add_argument("--extra-steps", type=int, default=40)
+    ap.add_argument("--base", default="prefill_base,prefill_base_l1024",
+                    help="fused base projection workloads (Eq. 1 whole) timed with lora_base_apply")
+    ap.add_argument("--base-steps", type=int, default=20)
     ap.add_argument("--rotate-mib", type=float, default=640.0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -246,11 +249,68 @@ def plan_update_cost(torch, w, dev, n=400):
                 plan_bytes=need)
 
 
+def measure_base(torch, name, dev, steps, rotate_mib):
+    """Eq. 1 whole (lora_base_apply: the shrink into float32 v, then the MFMA
+    GEMM of x . W with the delta in its epilogue) on R rotated copies of
+    {x, W, adapters, y}; the calls are timed between HIP events on their
+    stream (each call uploads its small work list, so it is not recorded)."""
+    from paper_2401_11240_amd import device as D
+    from paper_2401_11240_amd import lora as L
+    from paper_2401_11240_amd import workloads as W
+    w = W.BASE_NAMED[name]()
+    p0 = w.projections[0]
+    fp = footprint_bytes(w) + p0.W.nbytes
+    R = max(2, min(16, math.ceil(rotate_mib * 2 ** 20 / fp)))
+    log(f"[base] {w.name}: footprint {fp / 2**20:.1f} MiB, {R} rotated copies")
+    s = torch.cuda.current_stream(dev)
+    copies = []
+    for _ in range(R):
+        dw = D.upload(w, dev, stream=s)
+        wt = D.to_device_bits(np.ascontiguousarray(p0.W.T), dev)
+        p = dw.projections[0]
+        n = L.lora_base_workspace_bytes(p.table, dw.batch)
+        ws = torch.empty(n, dtype=torch.uint8, device=dev)
+        copies.append((dw, wt, ws, n))
+
+    def call(c):
+        dw, wt, ws, n = copies[c]
+        p = dw.projections[0]
+        x = dw.xs[p.x]
+        L.lora_base_apply(p.table, dw.batch, x, x.shape[1], wt, wt.shape[1], p.y, p.y.shape[1], ws, n, s)
+
+    for i in range(max(2, R)):
+        call(i % R)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    for i in range(steps):
+        call(i % R)
+    e1.record(s)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    for dw, *_ in copies:
+        dw.release()
+    del copies
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    M, K, N = w.n_rows, p0.h_in, p0.h_out
+    base_flops = 2 * M * K * N
+    flops = base_flops + W.algorithmic_flops(w)
+    tf = flops / (ms * 1e-3) / 1e12
+    return {
+        "workload": w.name, "tokens": M, "h_in": K, "h_out": N, "ms_per_step": ms,
+        "tokens_per_s": round(M / (ms * 1e-3), 1), "TFLOPs": round(tf, 2),
+        "pct_mfma_peak": round(100.0 * tf / MFMA_BF16_PEAK_TFLOPS, 2),
+        "algorithmic_flops_per_step": flops, "rotated_copies": R,
+        "timing": "HIP events around eager calls (shrink into v, then the fused GEMM)",
+    }
+
+
 def sources_hash() -> str:
     import hashlib
     csrc = os.path.join(ROOT, "paper_2401_11240_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("lora_api.hip", "lora_internal.h", "lora_kernels.hip"):
+    for f in ("lora_api.hip", "lora_internal.h", "lora_kernels.hip", "lora_device.h", "lora_base.hip"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -397,6 +457,11 @@ def main():
             "algorithmic_bytes_per_step": pre["bytes_per_step"],
             "rotated_copies": pre["R"],
         }
+    bases = [e for e in args.base.split(",") if e]
+    if bases:
+        out["base_fused"] = {}
+    for name in bases:
+        out["base_fused"][name] = measure_base(torch, name, dev, args.base_steps, args.rotate_mib)
     extras = [e for e in args.extra.split(",") if e]
     if extras:
         out["more"] = {}

@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define LORA_ABI_VERSION 3
+#define LORA_ABI_VERSION 4
 
 typedef enum { LORA_F16 = 0, LORA_BF16 = 1 } lora_dtype_t;
 
@@ -146,6 +146,33 @@ int lora_expand(lora_table_t t, const lora_batch_t* b, const float* v, int64_t l
  */
 int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,
                      int64_t ldy, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Eq. 1 whole (Section 2.1, y' = xW + xAB) for a step's rows, the base
+ * projection fused with the adapter delta (Section 4.1 folds the adapter into
+ * the base model's inference):
+ *
+ *     y[t, :] = round( x[t, :] . W  +  s_g (x[t, :] . A_g) . B_g )
+ *
+ * for every row t of the batch, g the adapter of its segment; rows of adapter
+ * -1 get round(x[t, :] . W).  y is OUTPUT only (every row is written, nothing
+ * is read from it).  The base weight is passed transposed: wt [h_out, ldw]
+ * row-major, row n holding column n of W (the layout of a linear layer's
+ * weight), ldw >= h_in and a multiple of 8, 16-byte aligned, spanning less
+ * than 2 GiB; the adapters are table t's (A_g [h_in, r_g], B_g [r_g, h_out]).
+ * The float32 x . A_g is computed first into ws (the shrink kernels), then one
+ * MFMA GEMM over tiles of 256 rows x 256 columns adds the delta in each tile's
+ * epilogue; results are rounded once.  Meant for prompt segments (rows of one
+ * adapter run together); decode tokens work, each adapter run of a tile
+ * costing one epilogue pass.  ws: device workspace of
+ * lora_base_workspace_bytes(t, b) bytes, any contents.  Uploads its work list
+ * through the same reused pinned ring as lora_apply_fused, so it refuses a
+ * capturing stream (LORA_E_CAPTURE).  Errors as lora_apply_fused's, plus wt
+ * and y must not overlap (LORA_E_OVERLAP).
+ */
+int lora_base_workspace_bytes(lora_table_t t, const lora_batch_t* b, size_t* bytes);
+int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, const void* wt,
+                    int64_t ldw, void* y, int64_t ldy, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * lora_apply_fused without a workspace argument and without allocating, for

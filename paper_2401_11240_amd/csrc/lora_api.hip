@@ -26,6 +26,7 @@ hipError_t launch_expand(const KernelArgs& a, const uint32_t* hdr, int dtype, hi
 hipError_t launch_reduce(const KernelArgs& a, const uint32_t* hdr, hipStream_t s);
 hipError_t launch_step(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s);
 hipError_t launch_fill(uint32_t* p, uint32_t v, uint64_t n_words, hipStream_t s);
+hipError_t launch_base(const BaseArgs& a, int dtype, hipStream_t s);
 }  // namespace lora
 
 using namespace lora;
@@ -927,6 +928,146 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
     unsigned char* w = (unsigned char*)ws;
     if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
     return enqueue(t, p, w, x, ldx, y, ldy, s);
+}
+
+// ---------------------------------------------------------------------------
+// fused base projection (Eq. 1 whole)
+// ---------------------------------------------------------------------------
+namespace {
+
+// Workspace of lora_base_apply: [plan (header, items, grouped rows) | partial
+// and v blocks | counters] [dense float32 v: n_rows x ldv] [per row tile:
+// offsets into the runs, then the runs of rows that share an adapter].
+struct BaseLayout {
+    HostPlan p;
+    int ldv = 8;
+    int n_mt = 0, n_nt = 0;
+    size_t off_v = 0, v_bytes = 0, off_pieces = 0, total = 0;
+    std::vector<unsigned char> pieces_blob;
+    size_t off_piece_list = 0;           // within pieces_blob
+};
+
+int build_base(const lora_table_s* t, const lora_batch_t* b, BaseLayout& L) {
+    if (int rc = build_plan(t, b, L.p)) return rc;
+    L.ldv = round_up_i(std::max(L.p.r_max, 1), 8);
+    L.off_v = align_up(L.p.total_bytes);
+    L.v_bytes = (size_t)b->n_rows * L.ldv * sizeof(float);
+    if (L.v_bytes > kMaxSpan) return fail(LORA_E_SHAPE, "batch too large: its float32 intermediate exceeds 2 GiB");
+    L.n_mt = (b->n_rows + kBaseBM - 1) / kBaseBM;
+    L.n_nt = (t->h_out + kBaseBN - 1) / kBaseBN;
+    // runs of rows sharing an adapter, per row tile; neighbouring segments of
+    // one adapter inside a tile make one run
+    std::vector<std::vector<BasePiece>> per(L.n_mt);
+    for (int sgi = 0; sgi < b->n_segments; ++sgi) {
+        const int g = b->seg_adapter[sgi];
+        int lo = b->seg_offset[sgi];
+        const int hi = b->seg_offset[sgi + 1];
+        if (g < 0) continue;
+        while (lo < hi) {
+            const int mt = lo / kBaseBM;
+            const int e = std::min(hi, (mt + 1) * kBaseBM);
+            auto& v = per[mt];
+            if (!v.empty() && v.back().adapter == g && v.back().hi == lo) v.back().hi = e;
+            else v.push_back(BasePiece{lo, e, g, 0});
+            lo = e;
+        }
+    }
+    std::vector<int32_t> off(L.n_mt + 1, 0);
+    for (int m = 0; m < L.n_mt; ++m) off[m + 1] = off[m] + (int32_t)per[m].size();
+    L.off_piece_list = align_up((size_t)(L.n_mt + 1) * sizeof(int32_t), 16);
+    L.pieces_blob.assign(L.off_piece_list + (size_t)off[L.n_mt] * sizeof(BasePiece), 0);
+    std::memcpy(L.pieces_blob.data(), off.data(), off.size() * sizeof(int32_t));
+    size_t at = L.off_piece_list;
+    for (const auto& v : per)
+        for (const BasePiece& pc : v) {
+            std::memcpy(L.pieces_blob.data() + at, &pc, sizeof pc);
+            at += sizeof pc;
+        }
+    L.off_pieces = align_up(L.off_v + L.v_bytes);
+    L.total = L.off_pieces + std::max<size_t>(L.pieces_blob.size(), 16);
+    return LORA_OK;
+}
+
+}  // namespace
+
+int lora_base_workspace_bytes(lora_table_t t, const lora_batch_t* b, size_t* bytes) {
+    if (int rc = check_table(t)) return rc;
+    if (!bytes) return fail(LORA_E_ARG, "bytes is NULL");
+    BaseLayout L;
+    if (int rc = build_base(t, b, L)) return rc;
+    *bytes = L.total;
+    return LORA_OK;
+}
+
+int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, const void* wt,
+                    int64_t ldw, void* y, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = check_table(t)) return rc;
+    BaseLayout L;
+    if (int rc = build_base(t, b, L)) return rc;
+    const int n_rows = b->n_rows;
+    if (n_rows == 0) return LORA_OK;
+    if (int rc = check_x(t, x, ldx, n_rows)) return rc;
+    if (int rc = check_y(t, y, ldy, n_rows)) return rc;
+    if (!wt) return fail(LORA_E_ARG, "wt is NULL");
+    if (!aligned16(wt)) return fail(LORA_E_ALIGN, "wt not 16-byte aligned");
+    if (int rc = check_ld("ldw", ldw, t->h_in)) return rc;
+    const uint64_t w_span = span_bytes(t->h_out, ldw, t->h_in);
+    if (w_span > kMaxSpan) return fail(LORA_E_SHAPE, "wt spans more than 2 GiB");
+    if (int rc = check_overlap(x, ldx, t->h_in, y, ldy, t->h_out, n_rows)) return rc;
+    {
+        const uintptr_t ws0 = (uintptr_t)wt, we = ws0 + w_span;
+        const uintptr_t ys = (uintptr_t)y, ye = ys + span_bytes(n_rows, ldy, t->h_out);
+        if (ws0 < ye && ys < we) return fail(LORA_E_OVERLAP, "wt and y overlap");
+    }
+    if (!ws) return fail(LORA_E_ARG, "workspace is NULL");
+    if (!aligned16(ws)) return fail(LORA_E_ALIGN, "workspace not 16-byte aligned");
+    if (ws_bytes < L.total)
+        return fail(LORA_E_WORKSPACE, "workspace has " + std::to_string(ws_bytes) + " bytes, needs " +
+                                          std::to_string(L.total));
+    DeviceGuard dg(t->device);
+    hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_base_apply")) return rc;
+    unsigned char* w = (unsigned char*)ws;
+    float* v = (float*)(w + L.off_v);
+    const HostPlan& p = L.p;
+    if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
+    if (int rc = stage_upload(t->device, L.pieces_blob.data(), L.pieces_blob.size(), w + L.off_pieces, s)) return rc;
+    if (p.n_active > 0) {
+        // v = x . A_g for every adapted row, into the dense float32 buffer
+        if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s, true)) return rc;
+        KernelArgs ra = make_args(t, p, w, kSpinLimit);
+        ra.items = (const DevItem*)(w + p.off_reduce_all);
+        ra.n_items = (int32_t)p.reduce_all.size();
+        ra.v = v;
+        ra.ldv = L.ldv;
+        LORA_HIP_TRY(launch_reduce(ra, (const uint32_t*)w, s));
+    }
+    BaseArgs a{};
+    a.x = x;
+    a.wt = wt;
+    a.y = y;
+    a.v = v;
+    a.table = t->dev;
+    a.piece_off = (const int32_t*)(w + L.off_pieces);
+    a.pieces = (const BasePiece*)(w + L.off_pieces + L.off_piece_list);
+    a.ldx = ldx;
+    a.ldw = ldw;
+    a.ldy = ldy;
+    a.ldv = L.ldv;
+    a.M = n_rows;
+    a.N = t->h_out;
+    a.K = t->h_in;
+    a.n_mt = L.n_mt;
+    a.n_nt = L.n_nt;
+    a.n_xcd = std::max(1, t->n_xcd);
+    a.per_xcd = (L.n_mt * L.n_nt + a.n_xcd - 1) / a.n_xcd;
+    a.x_bytes = (uint32_t)span_bytes(n_rows, ldx, t->h_in);
+    a.w_bytes = (uint32_t)w_span;
+    a.y_bytes = (uint32_t)span_bytes(n_rows, ldy, t->h_out);
+    a.v_bytes = (uint32_t)L.v_bytes;
+    a.b_span_ok = 1;
+    LORA_HIP_TRY(launch_base(a, t->dtype, s));
+    return LORA_OK;
 }
 
 int lora_apply_fused_static(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, void* y,

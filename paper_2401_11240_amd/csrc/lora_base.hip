@@ -1,0 +1,379 @@
+// gfx950 kernel of Eq. 1 whole (Section 2.1): the base projection and the
+// adapter delta of every row in one MFMA GEMM,
+//
+//     y[t, :] = round( x[t, :] . W  +  s_g (x[t, :] . A_g) . B_g ),
+//
+// where g is the adapter of row t's segment (rows of adapter -1 get x . W).
+// The float32 v = x . A_g comes in beforehand (the shrink kernels); the
+// delta s_g v . B_g is added in the epilogue of each output tile.  This is
+// the shape of a prompt step of Section 4.1's GPU LoRA once the base
+// projection is fused in: the base GEMM's arithmetic intensity is far above
+// the MFMA ridge, so the tile runs at MFMA rate while the delta costs r_g/K of
+// the base work.
+//
+// Tile: 256 rows of x (tokens) x 256 columns of y, one workgroup of 8 wave64
+// (2 x 4 waves, each 128 rows x 64 columns of the tile: 4 x 2 MFMA blocks of
+// 32 x 32, 128 float32 accumulators per lane).  The contraction runs on
+// v_mfma_f32_32x32x16 (measured here: about 34 cycles for its 32768 flop with
+// four independent accumulators, against about 27 for the 16384 of a
+// 16x16x32 even with sixteen) with the base weight as the A operand (rows =
+// output columns) and x as the B operand, so each group of four accumulators
+// holds four consecutive columns of one row of y (8-byte stores).
+//
+// The base weight is taken transposed, W^T [h_out, h_in] (row n = column n of
+// W, the layout of a linear layer's weight), so that both operands run along
+// K in memory: every 16-byte chunk of 8 consecutive K is one MFMA operand
+// slice, with no transpose.
+//
+// Pipeline: K advances in steps of 64, so that a row's slice of x or W is
+// one whole 128-byte line: eight consecutive lanes load one row slice
+// (16 bytes each), a wave eight whole rows per instruction.  (Loads of 32
+// bytes per row from 32 rows, in the operand's own order, measured about
+// 9 bytes per cycle per CU and bounded the kernel.)  The stage is loaded into
+// registers one step ahead and written to the other of two 64 KiB LDS
+// buffers in the order the MFMA operands are read: per 32-row block and
+// K-16 slice a 1 KiB region holding chunk c of row r at 32 (c % 2) + r % 32,
+// so the 64 lanes of an operand read one contiguous KiB, free of bank
+// conflicts.  Rows past the batch, columns past h_out and K past h_in are
+// loads out of the buffer's range, which read zeros.
+//
+// Epilogue: for every run of the tile's rows that share an adapter (at most
+// a few for prompt segments), B_g's ranks are staged in LDS 64 at a time,
+// transposed so that 8 consecutive ranks of one output column form an
+// operand slice, and each wave adds s_g v . B_g for its rows into its base
+// accumulators: s_g v is split into a high and a low 16-bit part that share
+// one 32x32x16 MFMA (its 16 K slots hold 8 ranks twice), rows of other runs
+// masked to zero.  binary16 cannot hold a high part past 65504, so for it each
+// wave first takes the largest |s_g v| it will use and, past 2^15, scales v
+// and its accumulators by a power of two around those MFMAs and back after
+// (exact).  The sum is rounded once to the storage dtype.
+//
+// Tiles go to XCDs in blocks: workgroup p runs on XCD p % n_xcd and takes the
+// (p / n_xcd)-th tile of that XCD's contiguous share of the row-major tile
+// order, so the tiles an XCD runs at a time share rows of x and columns of W
+// in its L2.
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#include "lora_device.h"
+#include "lora_internal.h"
+
+namespace lora {
+
+namespace {
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kStageChunks = kBaseStageBytes / 16;     // 4096 chunks of 16 bytes
+constexpr int kRegionChunks = 64;                      // one operand fragment: 32 rows x 2 chunks (K 16)
+constexpr int kKQ = kBaseBK / 16;                      // K-16 slices per stage
+constexpr int kWRegion = kKQ * (kBaseBM / 32);         // first region of the W slice in a stage
+constexpr int kRowChunks = kBaseBK / 8;                // 16-byte chunks per row of a stage
+constexpr int kLoads = (kBaseBM * kRowChunks) / kBaseThreads;   // chunks of x (and of W) a thread stages
+static_assert(kBaseBK == 64 && kBaseThreads == 512 && kBaseBM == kBaseBN, "base tiling");
+static_assert(kLoads == 4 && kBaseThreads % kRowChunks == 0, "staging");
+static_assert(kBaseLoraRanks * kBaseBN * 2 <= kBaseStageBytes, "B_g staging fits one stage buffer");
+
+// s_waitcnt lgkmcnt(0), vmcnt and expcnt left free (gfx9 encoding).
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+// s_waitcnt with lgkmcnt(0) and vmcnt(0).
+__device__ __forceinline__ void wait_vm0_lgkm0() { __builtin_amdgcn_s_waitcnt(0x0070); }
+
+// v_mfma_f32_32x32x16: A [32 x 16] lane l holds A[l % 32][8 (l / 32) .. +7];
+// B [16 x 32] lane l holds B[8 (l / 32) .. +7][l % 32]; accumulator r of
+// lane l is D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].
+template <class Fmt>
+__device__ __forceinline__ f32x16 mma32x32(const u32x4& a, const u32x4& b, f32x16 c);
+template <>
+__device__ __forceinline__ f32x16 mma32x32<FmtF16>(const u32x4& a, const u32x4& b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                  0, 0, 0);
+}
+template <>
+__device__ __forceinline__ f32x16 mma32x32<FmtBF16>(const u32x4& a, const u32x4& b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   c, 0, 0, 0);
+}
+
+template <class Fmt>
+struct BaseTile {
+    const BaseArgs& a;
+    const int t, w, l, wm, wn;
+    const int m0, n0;
+    rsrc_t xr, wr;
+    // this thread stages chunk c = t % 8 of rows r0 + 64 i (i < 4) of x and of W
+    int r0, c;
+    uint32_t xoff[kLoads], woff[kLoads];   // byte offsets at K = 0
+    u32x4 rx[kLoads], rw[kLoads];          // the next stage, in flight
+    f32x16 acc[4][2];                      // [32-row block of x][32-column block of y]
+
+    __device__ __forceinline__ BaseTile(const BaseArgs& args, int mt, int nt)
+        : a(args), t(threadIdx.x), w(threadIdx.x >> 6), l(threadIdx.x & 63), wm((threadIdx.x >> 6) >> 2),
+          wn((threadIdx.x >> 6) & 3), m0(mt * kBaseBM), n0(nt * kBaseBN) {
+        xr = make_rsrc(a.x, a.x_bytes);
+        wr = make_rsrc(a.wt, a.w_bytes);
+        r0 = t / kRowChunks;
+        c = t % kRowChunks;
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) {
+            const int row = m0 + r0 + 64 * i;
+            const int col = n0 + r0 + 64 * i;
+            xoff[i] = row < a.M ? (uint32_t)(((int64_t)row * a.ldx) * 2) + 16u * c : (uint32_t)kOut;
+            woff[i] = col < a.N ? (uint32_t)(((int64_t)col * a.ldw) * 2) + 16u * c : (uint32_t)kOut;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    }
+
+    // Stage k of x and W into registers: eight consecutive lanes read one
+    // 128-byte row slice, a wave eight whole rows per instruction.
+    __device__ __forceinline__ void load(int k) {
+        const bool kin = k * kBaseBK + 8 * c < a.K;    // K is a multiple of 8: whole chunks
+        const uint32_t kb = (uint32_t)k * (kBaseBK * 2);
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) {
+            rx[i] = bload16(xr, kin ? (int)(xoff[i] + kb) : kOut);
+            rw[i] = bload16(wr, kin ? (int)(woff[i] + kb) : kOut);
+        }
+    }
+
+    // The staged registers into buf, each chunk at its place in the operand
+    // order: chunk c of row r goes to region (r / 32, c / 2) at 32 (c % 2) +
+    // r % 32, its bits 1..3 flipped by 2c, so that the 16 chunks a quarter
+    // wave writes (two rows, eight chunks each) fall in 16 different bank
+    // groups.  A reader's 16 consecutive lanes share c and stay in one
+    // aligned group of 16 chunks.
+    __device__ __forceinline__ void commit(u32x4* buf) {
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) {
+            const int r = r0 + 64 * i;
+            const int pos = (kKQ * (r >> 5) + (c >> 1)) * kRegionChunks + ((32 * (c & 1) + (r & 31)) ^ (2 * c));
+            buf[pos] = rx[i];
+            buf[kWRegion * kRegionChunks + pos] = rw[i];
+        }
+    }
+
+    // One stage (K 64) on buf: per K-16 slice, its 6 operand reads, then its
+    // 8 MFMAs (the scheduler is kept from interleaving reads and MFMAs).
+    __device__ __forceinline__ void compute(const u32x4* buf) {
+        const int lsw = l ^ (2 * (l >> 5));       // lane l reads chunk 2q + l / 32 of its rows
+#pragma unroll
+        for (int q = 0; q < kKQ; ++q) {
+            u32x4 wf[2], xf[4];
+            const int ls = lsw ^ (4 * q);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) wf[j] = buf[(kWRegion + kKQ * (2 * wn + j) + q) * kRegionChunks + ls];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xf[i] = buf[(kKQ * (4 * wm + i) + q) * kRegionChunks + ls];
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = mma32x32<Fmt>(wf[j], xf[i], acc[i][j]);
+        }
+    }
+
+    // Step k: this wave's writes of stage k and reads of stage k-1 are done;
+    // meet the other waves; compute stage k; then write stage k+1 (loaded
+    // during step k-1) into the other buffer, whose readers have all passed
+    // this barrier, and start loading stage k+2.
+    __device__ __forceinline__ void step(const u32x4* cur, u32x4* nxt, int k, int nk) {
+        if (k >= nk) return;
+        wait_lgkm0();
+        __builtin_amdgcn_s_barrier();
+        compute(cur);
+        if (k + 1 < nk) {
+            commit(nxt);
+            if (k + 2 < nk) load(k + 2);
+        }
+    }
+};
+
+// The adapter delta of one run of rows [lo, hi) with adapter g, ranks staged
+// 64 at a time in bt (one stage buffer).
+template <class Fmt>
+__device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc, u32x4* bt) {
+    const BaseArgs& a = T.a;
+    const DevAdapter ad = a.table[pc.adapter];
+    const int R = ad.rank;
+    const rsrc_t br = make_rsrc(ad.B, (uint32_t)R * (uint32_t)a.N * 2u);
+    const rsrc_t vr = make_rsrc(a.v, a.v_bytes);
+    const int l = T.l;
+    for (int rc0 = 0; rc0 < R; rc0 += kBaseLoraRanks) {
+        const int rr = min_i(kBaseLoraRanks, R - rc0);
+        const int RC = (rr + 7) / 8;              // 8-rank chunks (one MFMA each)
+        // B_g ranks [rc0, rc0 + 8 RC) of the tile's columns into bt: column n
+        // of 32-column block nb, chunk c (ranks rc0 + 8c .. +7) at
+        // nb * 32 RC + 32 c + (n % 32).  A thread loads 8 columns of one rank
+        // (16 bytes) and writes each element to its place (2-byte LDS writes:
+        // few registers beside the accumulators).
+        __builtin_amdgcn_s_barrier();             // earlier readers of bt are done (every wave waited lgkmcnt)
+        uint16_t* bt16 = (uint16_t*)bt;
+        for (int task = T.t; task < 8 * RC * (kBaseBN / 8); task += kBaseThreads) {
+            const int jr = task / (kBaseBN / 8);  // rank within the staged range
+            const int co = task - jr * (kBaseBN / 8);
+            const int j = rc0 + jr;
+            const int col = T.n0 + 8 * co;
+            const u32x4 b8 = bload16(br, j < R && col < a.N ? (int)((((int64_t)j * a.N) + col) * 2) : kOut);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const int n = 8 * co + c;
+                const uint32_t word = b8[c >> 1];
+                bt16[((n >> 5) * (32 * RC) + 32 * (jr >> 3) + (n & 31)) * 8 + (jr & 7)] =
+                    (uint16_t)((c & 1) ? hi16(word) : lo16(word));
+            }
+        }
+        __syncthreads();
+        // v operand of block i, chunk c: lane l takes row m0 + 128 wm + 32 i + (l % 32),
+        // ranks rc0 + 8 c .. +7, the high part of s_g v for l < 32 and the low
+        // part for l >= 32 (the B_g operand holds the same ranks in both
+        // halves of K).  Rows outside [lo, hi) and ranks >= R read zero.
+        auto vload = [&](int i, int c, f32x4& v0, f32x4& v1) __attribute__((always_inline)) {
+            const int m = T.m0 + 128 * T.wm + 32 * i + (l & 31);
+            const int j = rc0 + 8 * c;
+            const bool ok = m >= pc.lo && m < pc.hi && j < R;
+            const int off = ok ? (int)((((int64_t)m * a.ldv) + j) * 4) : kOut;
+            v0 = as_f4(bload16(vr, off));
+            v1 = as_f4(bload16(vr, off + 16));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (j + e >= R) v0[e] = 0.f;
+                if (j + 4 + e >= R) v1[e] = 0.f;
+            }
+        };
+        // v enters the MFMA pre-multiplied by s_g, so the delta adds straight
+        // into the base accumulators.  binary16: past 2^15 the wave scales v
+        // by 2^k (k < 0) and its accumulators by 2^k around these MFMAs, then
+        // back by 2^-k; powers of two, exact for every accumulator at or above
+        // 2^-126+|k| (far below the output's precision).
+        float vmul = ad.scale;
+        float unscale = 1.f;
+        if constexpr (Fmt::kNarrowRange) {
+            float vabs = 0.f;
+            for (int i = 0; i < 4; ++i)
+                for (int c = 0; c < RC; ++c) {
+                    f32x4 v0, v1;
+                    vload(i, c, v0, v1);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        vabs = fmaxf(vabs, fmaxf(fabsf(v0[e] * ad.scale), fabsf(v1[e] * ad.scale)));
+                }
+#pragma unroll
+            for (int d = 32; d >= 1; d >>= 1) vabs = fmaxf(vabs, __shfl_xor(vabs, d, 64));
+            if (vabs >= 32768.f) {
+                const int E = (int)((__float_as_uint(vabs) >> 23) & 0xff) - 127;
+                const int k = max_i(14 - E, -64);
+                const float down = __uint_as_float((uint32_t)(127 + k) << 23);
+                vmul = ad.scale * down;
+                unscale = __uint_as_float((uint32_t)(127 - k) << 23);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int jn = 0; jn < 2; ++jn) T.acc[i][jn] *= down;
+            }
+        }
+        const bool hi_half = l < 32;
+        for (int c = 0; c < RC; ++c) {
+            u32x4 bf[2];
+#pragma unroll
+            for (int jn = 0; jn < 2; ++jn) bf[jn] = bt[(2 * T.wn + jn) * (32 * RC) + 32 * c + (l & 31)];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f32x4 v0, v1;
+                vload(i, c, v0, v1);
+                v0 *= vmul;
+                v1 *= vmul;
+                const uint32_t h0 = Fmt::pack2(v0[0], v0[1]), h1 = Fmt::pack2(v0[2], v0[3]);
+                const uint32_t h2 = Fmt::pack2(v1[0], v1[1]), h3 = Fmt::pack2(v1[2], v1[3]);
+                u32x4 vf;
+                if (hi_half) {
+                    vf = u32x4{h0, h1, h2, h3};
+                } else {
+                    vf = u32x4{Fmt::pack2(v0[0] - Fmt::to_f32(lo16(h0)), v0[1] - Fmt::to_f32(hi16(h0))),
+                               Fmt::pack2(v0[2] - Fmt::to_f32(lo16(h1)), v0[3] - Fmt::to_f32(hi16(h1))),
+                               Fmt::pack2(v1[0] - Fmt::to_f32(lo16(h2)), v1[1] - Fmt::to_f32(hi16(h2))),
+                               Fmt::pack2(v1[2] - Fmt::to_f32(lo16(h3)), v1[3] - Fmt::to_f32(hi16(h3)))};
+                }
+#pragma unroll
+                for (int jn = 0; jn < 2; ++jn) T.acc[i][jn] = mma32x32<Fmt>(bf[jn], vf, T.acc[i][jn]);
+            }
+        }
+        if constexpr (Fmt::kNarrowRange) {
+            if (unscale != 1.f) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int jn = 0; jn < 2; ++jn) T.acc[i][jn] *= unscale;
+            }
+        }
+        wait_vm0_lgkm0();                         // this wave's reads of bt are done before the next staging
+    }
+}
+
+template <class Fmt>
+__global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) {
+    __shared__ __attribute__((aligned(16))) u32x4 s0[kStageChunks];
+    __shared__ __attribute__((aligned(16))) u32x4 s1[kStageChunks];
+    const int p = blockIdx.x;
+    const int q = p / a.n_xcd;
+    const int tile = (p - q * a.n_xcd) * a.per_xcd + q;
+    if (q >= a.per_xcd || tile >= a.n_mt * a.n_nt) return;
+    const int mt = tile / a.n_nt;
+    const int nt = tile - mt * a.n_nt;
+    BaseTile<Fmt> T(a, mt, nt);
+
+    const int nk = (a.K + kBaseBK - 1) / kBaseBK;
+    T.load(0);
+    T.commit(s0);
+    if (nk > 1) T.load(1);
+    for (int k = 0; k < nk; k += 2) {
+        T.step(s0, s1, k, nk);
+        T.step(s1, s0, k + 1, nk);
+    }
+    wait_vm0_lgkm0();
+
+    // the adapter delta of each run of rows that carries one
+    const int pe = a.piece_off[mt + 1];
+    for (int pi = a.piece_off[mt]; pi < pe; ++pi) {
+        const BasePiece pc = a.pieces[pi];
+        tile_delta<Fmt>(T, pc, s0);
+    }
+
+    // y: accumulator r of block (i, j) is column n0 + 64 wn + 32 j + 8 (r / 4)
+    // + 4 (l / 32) + r % 4 of row m0 + 128 wm + 32 i + l % 32: four
+    // consecutive columns per group of four registers (8-byte stores)
+    const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int m = T.m0 + 128 * T.wm + 32 * i + (T.l & 31);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = T.n0 + 64 * T.wn + 32 * j + 8 * g + 4 * (T.l >> 5);
+                const bool ok = m < a.M && n < a.N;
+                const f32x16& c = T.acc[i][j];
+                bstore8(u32x2{Fmt::pack2(c[4 * g], c[4 * g + 1]), Fmt::pack2(c[4 * g + 2], c[4 * g + 3])}, yr,
+                        ok ? (int)((((int64_t)m * a.ldy) + n) * 2) : kOut);
+            }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_base(const BaseArgs& a, int dtype, hipStream_t s) {
+    const int grid = a.per_xcd * a.n_xcd;
+    if (grid <= 0) return hipSuccess;
+    if (dtype == 0)
+        hipLaunchKernelGGL(lora_base_kernel<FmtF16>, dim3(grid), dim3(kBaseThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(lora_base_kernel<FmtBF16>, dim3(grid), dim3(kBaseThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace lora

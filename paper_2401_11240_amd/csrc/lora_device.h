@@ -84,6 +84,10 @@ __device__ __forceinline__ u32x2 bload8(rsrc_t r, int off) {
     return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX));
 }
 template <int AUX = 0>
+__device__ __forceinline__ void bstore8(const u32x2& v, rsrc_t r, int off) {
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, AUX);
+}
+template <int AUX = 0>
 __device__ __forceinline__ void bstore16(const u32x4& v, rsrc_t r, int off) {
     __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, AUX);
 }

@@ -148,6 +148,39 @@ struct KernelArgs {
 static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 
 // ---------------------------------------------------------------------------
+// Fused base projection (Eq. 1 whole): y = x W + s_g (x A_g) B_g for every
+// row, one MFMA GEMM over tiles of kBaseBM rows x kBaseBN columns, the adapter
+// delta added in the tile's epilogue from a float32 v computed beforehand.
+// ---------------------------------------------------------------------------
+constexpr int kBaseBM = 256;             // rows of x (tokens) per tile
+constexpr int kBaseBN = 256;             // columns of y per tile
+constexpr int kBaseBK = 64;              // K per pipeline stage (one 128-byte line per row)
+constexpr int kBaseThreads = 512;        // 8 wave64: 2 (rows) x 4 (columns), 128 x 64 each
+constexpr int kBaseStageBytes = (kBaseBM + kBaseBN) * kBaseBK * 2;   // 64 KiB: x slice, then W slice
+constexpr int kBaseLoraRanks = 64;       // ranks of B_g staged in LDS at a time (one stage buffer)
+
+// One run of a tile's rows that share an adapter (g >= 0): rows [lo, hi).
+struct BasePiece {
+    int32_t lo, hi, adapter, pad;
+};
+
+struct BaseArgs {
+    const void* x;                 // [M, ldx] 16-bit
+    const void* wt;                // [N, ldw] 16-bit: the base weight transposed (row n = column n of W)
+    void* y;                       // [M, ldy] 16-bit, written
+    const float* v;                // [M, ldv] float32: v[t, 0:r_g] = x[t] . A_g
+    const DevAdapter* table;       // registry: B_g, rank, scale
+    const int32_t* piece_off;      // [n_mt + 1]: pieces of row tile mt are [piece_off[mt], piece_off[mt+1])
+    const BasePiece* pieces;
+    int64_t ldx, ldw, ldy, ldv;
+    int32_t M, N, K;               // rows, h_out, h_in
+    int32_t n_mt, n_nt;            // row tiles, column tiles
+    int32_t n_xcd, per_xcd;        // XCDs, tiles per XCD
+    uint32_t x_bytes, w_bytes, y_bytes, v_bytes;
+    int32_t b_span_ok;             // 1: every B_g spans < 2 GiB (checked on the host)
+};
+
+// ---------------------------------------------------------------------------
 // Tiling, shared by the planner (sizes the items) and the kernels (lay out
 // LDS).  All extents are in elements unless named *_bytes.
 // ---------------------------------------------------------------------------

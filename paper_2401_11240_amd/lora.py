@@ -40,6 +40,7 @@ EXPORTS = (
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
     "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
     "lora_plan_bytes", "lora_plan_create_reserved", "lora_plan_update", "lora_apply_fused_static",
+    "lora_base_workspace_bytes", "lora_base_apply",
     "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
 )
 
@@ -102,6 +103,8 @@ def load():
         "lora_expand": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_apply_fused": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, sz, vp],
         "lora_apply_fused_static": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp],
+        "lora_base_workspace_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
+        "lora_base_apply": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, i64, vp, sz, vp],
         "lora_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
         "lora_plan_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
         "lora_plan_create_reserved": [C.POINTER(vp), vp, C.POINTER(_Batch), sz, vp],
@@ -201,6 +204,19 @@ def lora_apply_fused(table: int, batch: Batch, x, ldx: int, y, ldy: int, ws, ws_
 def lora_apply_fused_static(table: int, batch: Batch, x, ldx: int, y, ldy: int, stream=None) -> None:
     """lora_apply_fused with the library's static scratch instead of a workspace."""
     _check(load().lora_apply_fused_static(table, batch.c, _addr(x), ldx, _addr(y), ldy, _stream(stream)))
+
+
+def lora_base_workspace_bytes(table: int, batch: Batch) -> int:
+    out = C.c_size_t()
+    _check(load().lora_base_workspace_bytes(table, batch.c, C.byref(out)))
+    return int(out.value)
+
+
+def lora_base_apply(table: int, batch: Batch, x, ldx: int, wt, ldw: int, y, ldy: int, ws, ws_bytes: int,
+                    stream=None) -> None:
+    """y = round(x . W + s_g (x . A_g) . B_g); ``wt`` is W transposed, [h_out, ldw]."""
+    _check(load().lora_base_apply(table, batch.c, _addr(x), ldx, _addr(wt), ldw, _addr(y), ldy, _addr(ws),
+                                  ws_bytes, _stream(stream)))
 
 
 def lora_plan_create(table: int, batch: Batch, stream=None) -> int:

@@ -31,6 +31,7 @@ hipError_t launch_expand(const KernelArgs&, const uint32_t*, int, hipStream_t) {
 hipError_t launch_reduce(const KernelArgs&, const uint32_t*, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_step(const KernelArgs&, const uint32_t*, int, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_fill(uint32_t*, uint32_t, uint64_t, hipStream_t) { return hipErrorNotSupported; }
+hipError_t launch_base(const BaseArgs&, int, hipStream_t) { return hipErrorNotSupported; }
 }  // namespace lora
 
 extern "C" {

@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version():
-    assert L.lora_abi_version() == 3
+    assert L.lora_abi_version() == 4
 
 
 def test_group_rows_hand_example_matches_golden():
