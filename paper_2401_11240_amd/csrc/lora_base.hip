@@ -70,15 +70,19 @@ constexpr int kRegionChunks = 64;                      // one operand fragment: 
 constexpr int kKQ = kBaseBK / 16;                      // K-16 slices per stage
 constexpr int kWRegion = kKQ * (kBaseBM / 32);         // first region of the W slice in a stage
 constexpr int kRowChunks = kBaseBK / 8;                // 16-byte chunks per row of a stage
-constexpr int kLoads = (kBaseBM * kRowChunks) / kBaseThreads;   // chunks of x (and of W) a thread stages
-static_assert(kBaseBK == 64 && kBaseThreads == 512 && kBaseBM == kBaseBN, "base tiling");
-static_assert(kLoads == 4 && kBaseThreads % kRowChunks == 0, "staging");
+constexpr int kRowStep = kBaseThreads / kRowChunks;    // rows between a thread's staged chunks
+constexpr int kLoads = kBaseBM / kRowStep;             // chunks of x (and of W) a thread stages
+static_assert(kBaseBK == 64 && kBaseThreads == 256 && kBaseBM == kBaseBN && kBaseBM == 256, "base tiling");
+static_assert(kLoads == 8 && kRowStep == 32, "staging");
 static_assert(kBaseLoraRanks * kBaseBN * 2 <= kBaseStageBytes, "B_g staging fits one stage buffer");
 
 // s_waitcnt lgkmcnt(0), vmcnt and expcnt left free (gfx9 encoding).
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 // s_waitcnt with lgkmcnt(0) and vmcnt(0).
 __device__ __forceinline__ void wait_vm0_lgkm0() { __builtin_amdgcn_s_waitcnt(0x0070); }
+
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100, kSchedDsWrite = 0x200;
 
 // v_mfma_f32_32x32x16: A [32 x 16] lane l holds A[l % 32][8 (l / 32) .. +7];
 // B [16 x 32] lane l holds B[8 (l / 32) .. +7][l % 32]; accumulator r of
@@ -102,95 +106,131 @@ struct BaseTile {
     const int t, w, l, wm, wn;
     const int m0, n0;
     rsrc_t xr, wr;
-    // this thread stages chunk c = t % 8 of rows r0 + 64 i (i < 4) of x and of W
-    int r0, c;
-    uint32_t xoff[kLoads], woff[kLoads];   // byte offsets at K = 0
-    u32x4 rx[kLoads], rw[kLoads];          // the next stage, in flight
-    f32x16 acc[4][2];                      // [32-row block of x][32-column block of y]
+    // this thread stages chunk c = t % 8 of rows r0 + 32 i (i < 8) of x and of W
+    int c;
+    uint32_t xo[kLoads], wo[kLoads];       // byte offsets at K = 0; kOut for rows past the matrix
+    int lpos;                              // LDS chunk of row r0 (region, swizzled lane)
+    u32x4 st[2][kLoads][2];                // the next two stages, in flight: [stage parity][i][x, W]
+    f32x16 acc[4][4];                      // [32-row block of x][32-column block of y]
 
     __device__ __forceinline__ BaseTile(const BaseArgs& args, int mt, int nt)
-        : a(args), t(threadIdx.x), w(threadIdx.x >> 6), l(threadIdx.x & 63), wm((threadIdx.x >> 6) >> 2),
-          wn((threadIdx.x >> 6) & 3), m0(mt * kBaseBM), n0(nt * kBaseBN) {
+        : a(args), t(threadIdx.x), w(threadIdx.x >> 6), l(threadIdx.x & 63), wm((threadIdx.x >> 6) >> 1),
+          wn((threadIdx.x >> 6) & 1), m0(mt * kBaseBM), n0(nt * kBaseBN) {
         xr = make_rsrc(a.x, a.x_bytes);
         wr = make_rsrc(a.wt, a.w_bytes);
-        r0 = t / kRowChunks;
+        const int r0 = t / kRowChunks;
         c = t % kRowChunks;
 #pragma unroll
         for (int i = 0; i < kLoads; ++i) {
-            const int row = m0 + r0 + 64 * i;
-            const int col = n0 + r0 + 64 * i;
-            xoff[i] = row < a.M ? (uint32_t)(((int64_t)row * a.ldx) * 2) + 16u * c : (uint32_t)kOut;
-            woff[i] = col < a.N ? (uint32_t)(((int64_t)col * a.ldw) * 2) + 16u * c : (uint32_t)kOut;
+            const int row = m0 + r0 + kRowStep * i, col = n0 + r0 + kRowStep * i;
+            xo[i] = row < a.M ? (uint32_t)(((int64_t)row * a.ldx) * 2) + 16u * c : (uint32_t)kOut;
+            wo[i] = col < a.N ? (uint32_t)(((int64_t)col * a.ldw) * 2) + 16u * c : (uint32_t)kOut;
         }
+        // chunk c of row r goes to region (r / 32, c / 2) at 32 (c % 2) + r % 32,
+        // its bits 1..3 flipped by 2c; rows r0 + 32 i are region rows i apart
+        lpos = (c >> 1) * kRegionChunks + ((32 * (c & 1) + r0) ^ (2 * c));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     }
 
-    // Stage k of x and W into registers: eight consecutive lanes read one
-    // 128-byte row slice, a wave eight whole rows per instruction.
+    // Stage k of x (part 0) or W (part 1) into staging set S: eight
+    // consecutive lanes read one 128-byte row slice, a wave eight whole rows
+    // per instruction.  Stages past K read zeros.
+    template <int S, int part>
     __device__ __forceinline__ void load(int k) {
-        const bool kin = k * kBaseBK + 8 * c < a.K;    // K is a multiple of 8: whole chunks
-        const uint32_t kb = (uint32_t)k * (kBaseBK * 2);
+        // one select per stage: K past the end moves every offset past the
+        // buffer (offsets and kOut stay below 2^32 together, above its size)
+        const uint32_t kb = k * kBaseBK + 8 * c < a.K ? (uint32_t)k * (kBaseBK * 2) : (uint32_t)kOut;
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
-            rx[i] = bload16(xr, kin ? (int)(xoff[i] + kb) : kOut);
-            rw[i] = bload16(wr, kin ? (int)(woff[i] + kb) : kOut);
-        }
+        for (int i = 0; i < kLoads; ++i) st[S][i][part] = bload16(part ? wr : xr, (int)((part ? wo[i] : xo[i]) + kb));
     }
 
-    // The staged registers into buf, each chunk at its place in the operand
-    // order: chunk c of row r goes to region (r / 32, c / 2) at 32 (c % 2) +
-    // r % 32, its bits 1..3 flipped by 2c, so that the 16 chunks a quarter
-    // wave writes (two rows, eight chunks each) fall in 16 different bank
-    // groups.  A reader's 16 consecutive lanes share c and stay in one
-    // aligned group of 16 chunks.
+    // The staged part 0 (x) or 1 (W) into buf in the operand order.  The
+    // 16 chunks a quarter wave writes (two rows, eight chunks each) fall in 16
+    // different bank groups; a reader's 16 consecutive lanes share c and stay
+    // in one aligned group of 16 chunks.
+    template <int S, int part>
     __device__ __forceinline__ void commit(u32x4* buf) {
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
-            const int r = r0 + 64 * i;
-            const int pos = (kKQ * (r >> 5) + (c >> 1)) * kRegionChunks + ((32 * (c & 1) + (r & 31)) ^ (2 * c));
-            buf[pos] = rx[i];
-            buf[kWRegion * kRegionChunks + pos] = rw[i];
-        }
+        for (int i = 0; i < kLoads; ++i) buf[(part ? kWRegion : 0) * kRegionChunks + i * (kKQ * kRegionChunks) + lpos] =
+            st[S][i][part];
     }
 
-    // One stage (K 64) on buf: per K-16 slice, its 6 operand reads, then its
-    // 8 MFMAs (the scheduler is kept from interleaving reads and MFMAs).
-    __device__ __forceinline__ void compute(const u32x4* buf) {
-        const int lsw = l ^ (2 * (l >> 5));       // lane l reads chunk 2q + l / 32 of its rows
+    // Operand fragments of K-16 slice q: W blocks 4 wn + j into f[0..3], x
+    // blocks 4 wm + i into f[4..7].
+    __device__ __forceinline__ void frags(const u32x4* buf, int q, u32x4* f) {
+        const int ls = (l ^ (2 * (l >> 5))) ^ (4 * q);   // lane l reads chunk 2q + l / 32 of its rows
 #pragma unroll
-        for (int q = 0; q < kKQ; ++q) {
-            u32x4 wf[2], xf[4];
-            const int ls = lsw ^ (4 * q);
+        for (int j = 0; j < 4; ++j) f[j] = buf[(kWRegion + kKQ * (4 * wn + j) + q) * kRegionChunks + ls];
 #pragma unroll
-            for (int j = 0; j < 2; ++j) wf[j] = buf[(kWRegion + kKQ * (2 * wn + j) + q) * kRegionChunks + ls];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) xf[i] = buf[(kKQ * (4 * wm + i) + q) * kRegionChunks + ls];
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) acc[i][j] = mma32x32<Fmt>(wf[j], xf[i], acc[i][j]);
-        }
+        for (int i = 0; i < 4; ++i) f[4 + i] = buf[(kKQ * (4 * wm + i) + q) * kRegionChunks + ls];
     }
 
-    // Step k: this wave's writes of stage k and reads of stage k-1 are done;
-    // meet the other waves; compute stage k; then write stage k+1 (loaded
-    // during step k-1) into the other buffer, whose readers have all passed
-    // this barrier, and start loading stage k+2.
-    __device__ __forceinline__ void step(const u32x4* cur, u32x4* nxt, int k, int nk) {
-        if (k >= nk) return;
+    __device__ __forceinline__ void mfmas(const u32x4* f) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = mma32x32<Fmt>(f[j], f[4 + i], acc[i][j]);
+    }
+
+    // Step k on buffer cur (stage k, written in step k-1).  Every wave's
+    // writes of stage k and reads of stage k-1 are done at the barrier; then
+    // the 64 MFMAs run with, in their shadow, the fragment reads of the next
+    // K slice, the writes of stage k+1 (loaded during step k-1) into nxt,
+    // whose readers have passed the barrier, and the loads of stage k+2.
+    template <int P>
+    __device__ __forceinline__ void step(const u32x4* cur, u32x4* nxt, int k) {
         wait_lgkm0();
         __builtin_amdgcn_s_barrier();
-        compute(cur);
-        if (k + 1 < nk) {
-            commit(nxt);
-            if (k + 2 < nk) load(k + 2);
+        u32x4 f[2][8];
+        frags(cur, 0, f[0]);
+        __builtin_amdgcn_sched_barrier(0);
+        // slice 0: 16 MFMAs, with the fragment reads of slice 1 and the x
+        // writes of stage k+1 between them
+        frags(cur, 1, f[1]);
+        commit<P ^ 1, 0>(nxt);
+        mfmas(f[0]);
+        for (int g = 0; g < 8; ++g) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
+        // slice 1: reads of slice 2, W writes of stage k+1
+        frags(cur, 2, f[0]);
+        commit<P ^ 1, 1>(nxt);
+        mfmas(f[1]);
+        for (int g = 0; g < 8; ++g) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // slice 2: reads of slice 3, x loads of stage k+3
+        frags(cur, 3, f[1]);
+        load<P ^ 1, 0>(k + 3);
+        mfmas(f[0]);
+        for (int g = 0; g < 8; ++g) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // slice 3: W loads of stage k+3
+        load<P ^ 1, 1>(k + 3);
+        mfmas(f[1]);
+        for (int g = 0; g < 8; ++g) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
     }
 };
 
@@ -274,14 +314,14 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int jn = 0; jn < 2; ++jn) T.acc[i][jn] *= down;
+                    for (int jn = 0; jn < 4; ++jn) T.acc[i][jn] *= down;
             }
         }
         const bool hi_half = l < 32;
         for (int c = 0; c < RC; ++c) {
-            u32x4 bf[2];
+            u32x4 bf[4];
 #pragma unroll
-            for (int jn = 0; jn < 2; ++jn) bf[jn] = bt[(2 * T.wn + jn) * (32 * RC) + 32 * c + (l & 31)];
+            for (int jn = 0; jn < 4; ++jn) bf[jn] = bt[(4 * T.wn + jn) * (32 * RC) + 32 * c + (l & 31)];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 f32x4 v0, v1;
@@ -300,7 +340,7 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
                                Fmt::pack2(v1[2] - Fmt::to_f32(lo16(h3)), v1[3] - Fmt::to_f32(hi16(h3)))};
                 }
 #pragma unroll
-                for (int jn = 0; jn < 2; ++jn) T.acc[i][jn] = mma32x32<Fmt>(bf[jn], vf, T.acc[i][jn]);
+                for (int jn = 0; jn < 4; ++jn) T.acc[i][jn] = mma32x32<Fmt>(bf[jn], vf, T.acc[i][jn]);
             }
         }
         if constexpr (Fmt::kNarrowRange) {
@@ -308,7 +348,7 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int jn = 0; jn < 2; ++jn) T.acc[i][jn] *= unscale;
+                    for (int jn = 0; jn < 4; ++jn) T.acc[i][jn] *= unscale;
             }
         }
         wait_vm0_lgkm0();                         // this wave's reads of bt are done before the next staging
@@ -327,13 +367,20 @@ __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) 
     const int nt = tile - mt * a.n_nt;
     BaseTile<Fmt> T(a, mt, nt);
 
-    const int nk = (a.K + kBaseBK - 1) / kBaseBK;
-    T.load(0);
-    T.commit(s0);
-    if (nk > 1) T.load(1);
+    // an even number of stages (a stage past K reads zeros and adds nothing),
+    // so that the loop runs whole pairs of steps and has one exit
+    const int nk = ((a.K + 2 * kBaseBK - 1) / (2 * kBaseBK)) * 2;
+    T.template load<0, 0>(0);
+    T.template load<0, 1>(0);
+    T.template load<1, 0>(1);
+    T.template load<1, 1>(1);
+    T.template commit<0, 0>(s0);
+    T.template commit<0, 1>(s0);
+    T.template load<0, 0>(2);
+    T.template load<0, 1>(2);
     for (int k = 0; k < nk; k += 2) {
-        T.step(s0, s1, k, nk);
-        T.step(s1, s0, k + 1, nk);
+        T.template step<0>(s0, s1, k);
+        T.template step<1>(s1, s0, k + 1);
     }
     wait_vm0_lgkm0();
 
@@ -352,10 +399,10 @@ __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) 
     for (int i = 0; i < 4; ++i) {
         const int m = T.m0 + 128 * T.wm + 32 * i + (T.l & 31);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int n = T.n0 + 64 * T.wn + 32 * j + 8 * g + 4 * (T.l >> 5);
+                const int n = T.n0 + 128 * T.wn + 32 * j + 8 * g + 4 * (T.l >> 5);
                 const bool ok = m < a.M && n < a.N;
                 const f32x16& c = T.acc[i][j];
                 bstore8(u32x2{Fmt::pack2(c[4 * g], c[4 * g + 1]), Fmt::pack2(c[4 * g + 2], c[4 * g + 3])}, yr,

@@ -155,7 +155,7 @@ static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 constexpr int kBaseBM = 256;             // rows of x (tokens) per tile
 constexpr int kBaseBN = 256;             // columns of y per tile
 constexpr int kBaseBK = 64;              // K per pipeline stage (one 128-byte line per row)
-constexpr int kBaseThreads = 512;        // 8 wave64: 2 (rows) x 4 (columns), 128 x 64 each
+constexpr int kBaseThreads = 256;        // 4 wave64: 2 (rows) x 2 (columns), 128 x 128 each
 constexpr int kBaseStageBytes = (kBaseBM + kBaseBN) * kBaseBK * 2;   // 64 KiB: x slice, then W slice
 constexpr int kBaseLoraRanks = 64;       // ranks of B_g staged in LDS at a time (one stage buffer)
 
