@@ -162,7 +162,10 @@ int lora_apply_fused(lora_table_t t, const lora_batch_t* b, const void* x, int64
  * than 2 GiB; the adapters are table t's (A_g [h_in, r_g], B_g [r_g, h_out]).
  * The float32 x . A_g is computed first into ws (the shrink kernels), then one
  * MFMA GEMM over tiles of 256 rows x 256 columns adds the delta in each tile's
- * epilogue; results are rounded once.  Meant for prompt segments (rows of one
+ * epilogue; results are rounded once.  The tiles of a last round that would
+ * leave compute units idle are split along h_in: their float32 partial tiles
+ * go to ws and a second kernel adds them in a fixed order (so results do not
+ * depend on timing), then rounds.  Meant for prompt segments (rows of one
  * adapter run together); decode tokens work, each adapter run of a tile
  * costing one epilogue pass.  ws: device workspace of
  * lora_base_workspace_bytes(t, b) bytes, any contents.  Uploads its work list

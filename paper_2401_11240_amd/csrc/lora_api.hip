@@ -81,6 +81,7 @@ struct DeviceGuard {
 struct lora_table_s {
     int device = 0;
     int n_xcd = 1;                      // XCDs of the device (workgroup p of a launch runs on XCD p % n_xcd)
+    int n_cu = 0;                       // compute units of the device
     int h_in = 0, h_out = 0, dtype = 0, n = 0;
     std::vector<DevAdapter> host;
     DevAdapter* dev = nullptr;
@@ -745,6 +746,9 @@ int lora_register_adapters(lora_table_t* out, int device, int h_in, int h_out, i
         int nx = 1;
         if (hipDeviceGetAttribute(&nx, hipDeviceAttributeNumberOfXccs, device) != hipSuccess || nx < 1) nx = 1;
         t->n_xcd = std::min(nx, 64);
+        int nc = 0;
+        if (hipDeviceGetAttribute(&nc, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) nc = 0;
+        t->n_cu = std::max(nc, 0);
     }
     t->h_in = h_in;
     t->h_out = h_out;
@@ -937,15 +941,40 @@ namespace {
 
 // Workspace of lora_base_apply: [plan (header, items, grouped rows) | partial
 // and v blocks | counters] [dense float32 v: n_rows x ldv] [per row tile:
-// offsets into the runs, then the runs of rows that share an adapter].
+// offsets into the runs, then the runs of rows that share an adapter]
+// [float32 partial tiles of the split tiles].
 struct BaseLayout {
     HostPlan p;
     int ldv = 8;
     int n_mt = 0, n_nt = 0;
-    size_t off_v = 0, v_bytes = 0, off_pieces = 0, total = 0;
+    int n_whole = 0, split = 1, chunk = 0;
+    size_t off_v = 0, v_bytes = 0, off_pieces = 0, off_part = 0, part_bytes = 0, total = 0;
     std::vector<unsigned char> pieces_blob;
     size_t off_piece_list = 0;           // within pieces_blob
 };
+
+// Work of one launch: whole rounds of tiles over the compute units run whole;
+// the tiles of a last, partial round are split along K into ranges of at
+// least kBaseMinSplitStages stages (an even number of them), as many as fill
+// the compute units, their partial tiles added by a second kernel.
+void choose_split(int n_tiles, int h_in, int n_cu, BaseLayout& L) {
+    const int nk = ((h_in + 2 * kBaseBK - 1) / (2 * kBaseBK)) * 2;
+    L.n_whole = n_tiles;
+    L.split = 1;
+    L.chunk = nk;
+    if (n_cu <= 0 || n_tiles == 0) return;
+    const int rounds = n_tiles / n_cu;
+    const int rem = n_tiles - rounds * n_cu;
+    if (rem == 0) return;
+    const int s = std::min(n_cu / rem, nk / kBaseMinSplitStages);
+    if (s < 2) return;
+    const int chunk = round_up_i((nk + s - 1) / s, 2);
+    const int split = (nk + chunk - 1) / chunk;
+    if (split < 2) return;
+    L.n_whole = rounds * n_cu;
+    L.split = split;
+    L.chunk = chunk;
+}
 
 int build_base(const lora_table_s* t, const lora_batch_t* b, BaseLayout& L) {
     if (int rc = build_plan(t, b, L.p)) return rc;
@@ -984,7 +1013,11 @@ int build_base(const lora_table_s* t, const lora_batch_t* b, BaseLayout& L) {
             at += sizeof pc;
         }
     L.off_pieces = align_up(L.off_v + L.v_bytes);
-    L.total = L.off_pieces + std::max<size_t>(L.pieces_blob.size(), 16);
+    L.off_part = align_up(L.off_pieces + std::max<size_t>(L.pieces_blob.size(), 16));
+    choose_split(L.n_mt * L.n_nt, t->h_in, t->n_cu, L);
+    L.part_bytes = (size_t)(L.n_mt * L.n_nt - L.n_whole) * L.split * (kBaseBM * kBaseBN * sizeof(float));
+    if (L.split < 2) L.part_bytes = 0;
+    L.total = L.off_part + L.part_bytes;
     return LORA_OK;
 }
 
@@ -1060,7 +1093,11 @@ int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_
     a.n_mt = L.n_mt;
     a.n_nt = L.n_nt;
     a.n_xcd = std::max(1, t->n_xcd);
-    a.per_xcd = (L.n_mt * L.n_nt + a.n_xcd - 1) / a.n_xcd;
+    a.n_whole = L.n_whole;
+    a.per_xcd = (L.n_whole + a.n_xcd - 1) / a.n_xcd;
+    a.split = L.split;
+    a.chunk = L.chunk;
+    a.part = L.split > 1 ? (float*)(w + L.off_part) : nullptr;
     a.x_bytes = (uint32_t)span_bytes(n_rows, ldx, t->h_in);
     a.w_bytes = (uint32_t)w_span;
     a.y_bytes = (uint32_t)span_bytes(n_rows, ldy, t->h_out);

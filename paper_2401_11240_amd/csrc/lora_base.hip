@@ -359,39 +359,68 @@ template <class Fmt>
 __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) {
     __shared__ __attribute__((aligned(16))) u32x4 s0[kStageChunks];
     __shared__ __attribute__((aligned(16))) u32x4 s1[kStageChunks];
+    // an even number of stages (a stage past K reads zeros and adds nothing),
+    // so that the loop runs whole pairs of steps and has one exit
+    const int nk = ((a.K + 2 * kBaseBK - 1) / (2 * kBaseBK)) * 2;
     const int p = blockIdx.x;
-    const int q = p / a.n_xcd;
-    const int tile = (p - q * a.n_xcd) * a.per_xcd + q;
-    if (q >= a.per_xcd || tile >= a.n_mt * a.n_nt) return;
+    int tile, k0 = 0, k1 = nk, range = -1;
+    if (p < a.n_whole) {
+        const int q = p / a.n_xcd;
+        tile = (p - q * a.n_xcd) * a.per_xcd + q;
+        if (q >= a.per_xcd || tile >= a.n_whole) return;
+    } else {
+        const int u = p - a.n_whole;
+        tile = a.n_whole + u / a.split;
+        range = u - (tile - a.n_whole) * a.split;
+        k0 = range * a.chunk;
+        k1 = min_i(nk, k0 + a.chunk);
+        if (tile >= a.n_mt * a.n_nt || k0 >= k1) return;
+    }
     const int mt = tile / a.n_nt;
     const int nt = tile - mt * a.n_nt;
     BaseTile<Fmt> T(a, mt, nt);
 
-    // an even number of stages (a stage past K reads zeros and adds nothing),
-    // so that the loop runs whole pairs of steps and has one exit
-    const int nk = ((a.K + 2 * kBaseBK - 1) / (2 * kBaseBK)) * 2;
-    T.template load<0, 0>(0);
-    T.template load<0, 1>(0);
-    T.template load<1, 0>(1);
-    T.template load<1, 1>(1);
+    T.template load<0, 0>(k0);
+    T.template load<0, 1>(k0);
+    T.template load<1, 0>(k0 + 1);
+    T.template load<1, 1>(k0 + 1);
     T.template commit<0, 0>(s0);
     T.template commit<0, 1>(s0);
-    T.template load<0, 0>(2);
-    T.template load<0, 1>(2);
-    for (int k = 0; k < nk; k += 2) {
+    T.template load<0, 0>(k0 + 2);
+    T.template load<0, 1>(k0 + 2);
+    for (int k = k0; k < k1; k += 2) {
         T.template step<0>(s0, s1, k);
         T.template step<1>(s1, s0, k + 1);
     }
     wait_vm0_lgkm0();
 
-    // the adapter delta of each run of rows that carries one
-    const int pe = a.piece_off[mt + 1];
-    for (int pi = a.piece_off[mt]; pi < pe; ++pi) {
-        const BasePiece pc = a.pieces[pi];
-        tile_delta<Fmt>(T, pc, s0);
+    // the adapter delta of each run of rows that carries one (once per tile)
+    if (range <= 0) {
+        const int pe = a.piece_off[mt + 1];
+        for (int pi = a.piece_off[mt]; pi < pe; ++pi) {
+            const BasePiece pc = a.pieces[pi];
+            tile_delta<Fmt>(T, pc, s0);
+        }
     }
 
-    // y: accumulator r of block (i, j) is column n0 + 64 wn + 32 j + 8 (r / 4)
+    if (range >= 0) {
+        // partial tile in accumulator order: float4 g of block (i, j) of wave
+        // w, lane l at (((w 4 + i) 4 + j) 4 + g) 64 + l
+        float4* dst = (float4*)a.part + (size_t)((tile - a.n_whole) * a.split + range) * (kBaseBM * kBaseBN / 4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x16& c = T.acc[i][j];
+                    dst[(((T.w * 4 + i) * 4 + j) * 4 + g) * 64 + T.l] =
+                        float4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+                }
+        return;
+    }
+
+    // y: accumulator r of block (i, j) is column n0 + 128 wn + 32 j + 8 (r / 4)
     // + 4 (l / 32) + r % 4 of row m0 + 128 wm + 32 i + l % 32: four
     // consecutive columns per group of four registers (8-byte stores)
     const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
@@ -411,15 +440,56 @@ __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) 
     }
 }
 
+// The split tiles: the float32 partials of ranges 0 .. split-1 added in that
+// order, rounded once and stored.  One thread per four consecutive columns of
+// one row (one float4 of every partial).
+constexpr int kReduceThreads = 256;
+constexpr int kTileQuads = kBaseBM * kBaseBN / 4;
+static_assert(kTileQuads % kReduceThreads == 0, "reduce grid");
+
+template <class Fmt>
+__global__ void __launch_bounds__(kReduceThreads) lora_base_reduce_kernel(BaseArgs a) {
+    const int gid = blockIdx.x * kReduceThreads + threadIdx.x;
+    const int rt = gid / kTileQuads;
+    const int e = gid - rt * kTileQuads;
+    const int l = e & 63, g = (e >> 6) & 3, j = (e >> 8) & 3, i = (e >> 10) & 3, w = e >> 12;
+    const int tile = a.n_whole + rt;
+    if (tile >= a.n_mt * a.n_nt) return;
+    const int mt = tile / a.n_nt, nt = tile - mt * a.n_nt;
+    const int m = mt * kBaseBM + 128 * (w >> 1) + 32 * i + (l & 31);
+    const int n = nt * kBaseBN + 128 * (w & 1) + 32 * j + 8 * g + 4 * (l >> 5);
+    const float4* src = (const float4*)a.part + (size_t)rt * a.split * kTileQuads + e;
+    float4 sum = src[0];
+    for (int r = 1; r < a.split; ++r) {
+        const float4 v = src[(size_t)r * kTileQuads];
+        sum.x += v.x;
+        sum.y += v.y;
+        sum.z += v.z;
+        sum.w += v.w;
+    }
+    if (m < a.M && n < a.N) {
+        const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
+        bstore8(u32x2{Fmt::pack2(sum.x, sum.y), Fmt::pack2(sum.z, sum.w)}, yr, (int)((((int64_t)m * a.ldy) + n) * 2));
+    }
+}
+
 }  // namespace
 
 hipError_t launch_base(const BaseArgs& a, int dtype, hipStream_t s) {
-    const int grid = a.per_xcd * a.n_xcd;
+    const int n_split = a.split > 1 ? a.n_mt * a.n_nt - a.n_whole : 0;
+    const int grid = a.n_whole + n_split * a.split;
     if (grid <= 0) return hipSuccess;
     if (dtype == 0)
         hipLaunchKernelGGL(lora_base_kernel<FmtF16>, dim3(grid), dim3(kBaseThreads), 0, s, a);
     else
         hipLaunchKernelGGL(lora_base_kernel<FmtBF16>, dim3(grid), dim3(kBaseThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n_split == 0) return e;
+    const int rgrid = n_split * (kTileQuads / kReduceThreads);
+    if (dtype == 0)
+        hipLaunchKernelGGL(lora_base_reduce_kernel<FmtF16>, dim3(rgrid), dim3(kReduceThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(lora_base_reduce_kernel<FmtBF16>, dim3(rgrid), dim3(kReduceThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -157,6 +157,7 @@ constexpr int kBaseBN = 256;             // columns of y per tile
 constexpr int kBaseBK = 64;              // K per pipeline stage (one 128-byte line per row)
 constexpr int kBaseThreads = 256;        // 4 wave64: 2 (rows) x 2 (columns), 128 x 128 each
 constexpr int kBaseStageBytes = (kBaseBM + kBaseBN) * kBaseBK * 2;   // 64 KiB: x slice, then W slice
+constexpr int kBaseMinSplitStages = 8;   // fewest K stages of a split range
 constexpr int kBaseLoraRanks = 64;       // ranks of B_g staged in LDS at a time (one stage buffer)
 
 // One run of a tile's rows that share an adapter (g >= 0): rows [lo, hi).
@@ -175,7 +176,14 @@ struct BaseArgs {
     int64_t ldx, ldw, ldy, ldv;
     int32_t M, N, K;               // rows, h_out, h_in
     int32_t n_mt, n_nt;            // row tiles, column tiles
-    int32_t n_xcd, per_xcd;        // XCDs, tiles per XCD
+    int32_t n_xcd, per_xcd;        // XCDs, whole tiles per XCD
+    // Tiles [0, n_whole) run whole, one workgroup each.  Each tile of
+    // [n_whole, n_mt n_nt) is split into `split` K ranges of `chunk` stages
+    // (workgroup n_whole + (tile - n_whole) split + s takes range s), which
+    // write float32 partial tiles to `part`; a second kernel adds them in the
+    // order of s, rounds and stores.  Range 0 carries the adapter delta.
+    int32_t n_whole, split, chunk;
+    float* part;                   // [(n_mt n_nt - n_whole) split][kBaseBM kBaseBN] in accumulator order
     uint32_t x_bytes, w_bytes, y_bytes, v_bytes;
     int32_t b_span_ok;             // 1: every B_g spans < 2 GiB (checked on the host)
 };
