@@ -73,6 +73,8 @@ def parse():
     ap.add_argument("--base", default="prefill_base,prefill_base_l1024",
                     help="fused base projection workloads (Eq. 1 whole) timed with lora_base_apply")
     ap.add_argument("--base-steps", type=int, default=20)
+    ap.add_argument("--costmodel-steps", type=int, default=96,
+                    help="decode launches timed per point of the cost-model sweep (0: skip the sweep)")
     ap.add_argument("--rotate-mib", type=float, default=640.0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -483,6 +485,23 @@ def main():
             "rotated_copies": mx["R"],
         }
         del wx
+    if args.costmodel_steps > 0:
+        from paper_2401_11240_amd import costmodel as CM
+        log("[costmodel] decode sweep over batch sizes x rank mixes")
+        pts = CM.decode_sweep(torch, dev, steps=args.costmodel_steps)
+        fits = CM.fit(pts)
+        log("[costmodel] simulating the routing policies")
+        sims = {}
+        for kind in ("sum_rank", "padded"):
+            pre_m, dec_m = CM.serving_models(fits, kind)
+            sims[kind] = CM.simulate_policies(pre_m, dec_m)
+            sims[kind]["models_ms"] = {"decode": list(dec_m.as_tuple()), "prefill": list(pre_m.as_tuple())}
+        out["cost_model"] = {
+            "projection": f"{CM.H_IN}->{CM.H_OUT} f16 decode step launch, one adapter per request",
+            "fit_us": fits,
+            "points": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in p.items()} for p in pts],
+            "simulation": sims,
+        }
     if args.calibrate_copy_mib > 0:
         n = int(args.calibrate_copy_mib * 2 ** 20)
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)

@@ -27,6 +27,7 @@ hipError_t launch_reduce(const KernelArgs& a, const uint32_t* hdr, hipStream_t s
 hipError_t launch_step(const KernelArgs& a, const uint32_t* hdr, int dtype, hipStream_t s);
 hipError_t launch_fill(uint32_t* p, uint32_t v, uint64_t n_words, hipStream_t s);
 hipError_t launch_base(const BaseArgs& a, int dtype, hipStream_t s);
+int set_error(int code, const std::string& msg);
 }  // namespace lora
 
 using namespace lora;
@@ -39,6 +40,13 @@ int fail(int code, const std::string& msg) {
     g_err = msg;
     return code;
 }
+
+}  // namespace
+
+// the same thread-local message for the library's other host sources
+int lora::set_error(int code, const std::string& msg) { return fail(code, msg); }
+
+namespace {
 
 #define LORA_HIP_TRY(expr)                                                                    \
     do {                                                                                      \

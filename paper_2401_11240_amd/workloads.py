@@ -421,3 +421,30 @@ def adapter_bytes_per_rank(shapes: Sequence[tuple], n_layers: int, elem_bytes: i
     """Bytes of one unit of rank for adapters on the given (h_in, h_out)
     projections of every layer."""
     return n_layers * sum((a + b) for a, b in shapes) * elem_bytes
+
+
+# ---------------------------------------------------------------------------
+# request traces for the scheduling simulation
+# ---------------------------------------------------------------------------
+
+def sim_trace(seed: int, n: int, rps: float, *, n_adapters: int = 64, rank_pool: Sequence[int] = (8, 16, 32, 64),
+              zipf_s: float = 1.1, prompt: tuple = (16, 512), output: tuple = (16, 256)) -> List[dict]:
+    """A seeded synthetic request trace (stand-in for a production trace):
+    Poisson arrivals at ``rps`` requests per second, adapters drawn with Zipf
+    popularity from a pool whose ranks are drawn uniformly from ``rank_pool``,
+    prompt and output lengths uniform over the given inclusive ranges, and one
+    uniform [0, 1) draw per request for a random router.
+
+    Draw order, one ``numpy.random.default_rng(seed)``: adapter ranks,
+    inter-arrival gaps, adapters, prompt lengths, output lengths, uniforms.
+    Times are in milliseconds."""
+    rng = np.random.default_rng(seed)
+    ranks = rng.choice(np.asarray(rank_pool, dtype=np.int32), size=n_adapters)
+    gaps = rng.exponential(1000.0 / rps, size=n)
+    adapters = rng.choice(n_adapters, size=n, p=zipf_probs(n_adapters, zipf_s))
+    prompts = rng.integers(prompt[0], prompt[1] + 1, size=n)
+    outputs = rng.integers(output[0], output[1] + 1, size=n)
+    us = rng.random(size=n)
+    t = np.cumsum(gaps)
+    return [dict(arrival=float(t[i]), rank=int(ranks[adapters[i]]), prompt=int(prompts[i]),
+                 output=int(outputs[i]), u=float(us[i]), adapter=int(adapters[i])) for i in range(n)]

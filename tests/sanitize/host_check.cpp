@@ -21,6 +21,7 @@
 
 #include "lora.h"
 #include "lora_internal.h"
+#include "lora_sched.h"
 
 // The planner's launch functions live with the kernels, which this build
 // leaves out: nothing here launches (every call exercised returns before any
@@ -275,6 +276,44 @@ void check_oracle() {
     }
 }
 
+// the scheduler's simulator and cost score on random traces: every request
+// routed to a valid instance, times ordered, no memory error
+void check_sched(int reps) {
+    for (int rep = 0; rep < reps; ++rep) {
+        const int n = rint_in(0, 400);
+        std::vector<lora_sim_req_t> q(n);
+        double t = 0.0;
+        for (int j = 0; j < n; ++j) {
+            t += (double)rint_in(0, 50) * 0.1;
+            q[j] = lora_sim_req_t{t, 8 << rint_in(0, 3), rint_in(1, 300), rint_in(1, 40), 0, (double)rint_in(0, 999) / 1000.0};
+        }
+        lora_sim_config_t c{};
+        c.pre = lora_perf_model_t{LORA_PERF_TOKENS, 0, 0.01, 0.5};
+        c.dec = lora_perf_model_t{rint_in(0, 1), 0, 0.002, 3.0};
+        c.n_instances = rint_in(1, 12);
+        c.max_batch = rint_in(1, 20);
+        c.policy = rint_in(0, 3);
+        c.avg_resp_len = 20.0;
+        c.slo = 4.0;
+        c.penalty = 100.0;
+        std::vector<lora_sim_out_t> o(n);
+        const int rc = lora_sim_run(&c, q.data(), n, o.data());
+        CHECK(rc == LORA_OK, "lora_sim_run: %d %s", rc, lora_last_error());
+        for (int j = 0; j < n; ++j) {
+            CHECK(o[j].instance >= 0 && o[j].instance < c.n_instances, "request %d on instance %d", j, o[j].instance);
+            CHECK(o[j].first_token >= q[j].arrival && o[j].finish >= o[j].first_token, "request %d times", j);
+        }
+        std::vector<lora_req_t> run(rint_in(0, 30)), qq(rint_in(0, 5));
+        for (auto& r : run) r = lora_req_t{rint_in(1, 256), rint_in(1, 100)};
+        for (auto& r : qq) r = lora_req_t{rint_in(1, 256), rint_in(1, 100)};
+        const lora_req_t req{rint_in(1, 256), rint_in(1, 100)};
+        const double cost = lora_sched_cost(&c.pre, &c.dec, &req, run.data(), (int32_t)run.size(), qq.data(),
+                                            (int32_t)qq.size(), 10.0, 5.0, 1.0);
+        CHECK(cost == cost, "lora_sched_cost gave NaN");
+    }
+    CHECK(lora_sim_run(nullptr, nullptr, 0, nullptr) == LORA_E_ARG, "NULL configuration accepted");
+}
+
 }  // namespace
 
 int main() {
@@ -286,6 +325,7 @@ int main() {
     }
     check_errors(7);
     check_oracle();
+    check_sched(200);
     if (failures) {
         std::fprintf(stderr, "%d checks failed\n", failures);
         return 1;

@@ -28,8 +28,17 @@ def header_functions():
     return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(lora_\w+)\s*\(", text, flags=re.M)))
 
 
+def sched_header_functions():
+    with open(os.path.join(ROOT, "include", "lora_sched.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|double)\s+(lora_\w+)\s*\(", text, flags=re.M)))
+
+
 def test_header_and_binding_agree():
     assert header_functions() == sorted(L.EXPORTS)
+    from paper_2401_11240_amd import sched as SC
+    assert sched_header_functions() == sorted(SC.EXPORTS)
 
 
 def test_library_exports_every_declared_symbol():
@@ -41,7 +50,7 @@ def test_library_exports_every_declared_symbol():
     out = subprocess.run(["nm", "-D", "--defined-only", B.lib_path()], capture_output=True,
                          text=True, check=True).stdout
     syms = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
-    for name in header_functions():
+    for name in header_functions() + sched_header_functions():
         assert name in syms, name
 
 

@@ -1,4 +1,4 @@
-"""The library's host code (validation, grouping, planner) and the oracle
+"""The library's host code (validation, grouping, planner, scheduler) and the oracle
 built with AddressSanitizer and UndefinedBehaviorSanitizer, exercised on
 random batches by tests/sanitize/host_check.cpp.  CPU only: nothing is
 launched on a GPU (the device code is compiled as usual and never run)."""
@@ -35,6 +35,11 @@ def test_planner_and_oracle_under_asan_ubsan(tmp_path):
                               f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"] + B.DEVICE_FLAGS + host_san +
                              [src, "-o", objs[-1]], capture_output=True, text=True)
         assert res.returncode == 0, res.stderr[-4000:]
+    # the scheduler: plain C++
+    objs.append(str(tmp_path / "lora_sched.o"))
+    res = subprocess.run([CLANGXX, "-c", "-O1", "-g", "-std=c++17", f"-I{os.path.join(ROOT, 'include')}"] + san +
+                         [os.path.join(CSRC, "lora_sched.cpp"), "-o", objs[-1]], capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr[-4000:]
     exe = str(tmp_path / "host_check")
     res = subprocess.run([CLANGXX] + san + objs + ["-L/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib", "-lamdhip64",
                                                    "-o", exe], capture_output=True, text=True)
