@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblora.so")
-SOURCES = ["lora_api.hip", "lora_kernels.hip", "lora_base.hip", "lora_sched.cpp"]
+SOURCES = ["lora_api.hip", "lora_kernels.hip", "lora_base.hip", "lora_cold.hip", "lora_sched.cpp", "lora_cpu.cpp"]
 ARCH = "gfx950"
 
 # Packed-FP32 VALU forms are kept out of the device code; the host pass warns

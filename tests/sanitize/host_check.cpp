@@ -22,6 +22,7 @@
 #include "lora.h"
 #include "lora_internal.h"
 #include "lora_sched.h"
+#include "lora_coldstart.h"
 
 // The planner's launch functions live with the kernels, which this build
 // leaves out: nothing here launches (every call exercised returns before any
@@ -314,6 +315,26 @@ void check_sched(int reps) {
     CHECK(lora_sim_run(nullptr, nullptr, 0, nullptr) == LORA_E_ARG, "NULL configuration accepted");
 }
 
+// the CPU LoRA kernel on random shapes and thread splits: no memory error,
+// the same result for every split
+void check_cpu_delta(int reps) {
+    for (int rep = 0; rep < reps; ++rep) {
+        const int T = rint_in(0, 40), h_in = 8 * rint_in(1, 40), h_out = 8 * rint_in(1, 40), r = rint_in(1, 64);
+        const int dtype = rint_in(0, 1);
+        std::vector<uint16_t> x((size_t)T * h_in + 1), A((size_t)h_in * r), Bm((size_t)r * h_out);
+        for (auto& e : x) e = (uint16_t)(dtype ? 0x3c00 + rint_in(0, 255) : 0x3800 + rint_in(0, 511));
+        for (auto& e : A) e = (uint16_t)(dtype ? 0x3c00 + rint_in(0, 255) : 0x3800 + rint_in(0, 511));
+        for (auto& e : Bm) e = (uint16_t)(dtype ? 0x3c00 + rint_in(0, 255) : 0x3800 + rint_in(0, 511));
+        std::vector<float> d1((size_t)T * h_out + 1), d2((size_t)T * h_out + 1);
+        int rc = lora_cpu_delta(x.data(), h_in, T, h_in, h_out, dtype, A.data(), Bm.data(), r, 0.5f, d1.data(), h_out, 0, 1);
+        CHECK(rc == LORA_OK, "lora_cpu_delta: %d %s", rc, lora_last_error());
+        rc = lora_cpu_delta(x.data(), h_in, T, h_in, h_out, dtype, A.data(), Bm.data(), r, 0.5f, d2.data(), h_out,
+                            rint_in(1, 9), rint_in(1, 8));
+        CHECK(rc == LORA_OK, "lora_cpu_delta threads: %d %s", rc, lora_last_error());
+        CHECK(std::memcmp(d1.data(), d2.data(), sizeof(float) * (size_t)T * h_out) == 0, "thread split changed the result");
+    }
+}
+
 }  // namespace
 
 int main() {
@@ -326,6 +347,7 @@ int main() {
     check_errors(7);
     check_oracle();
     check_sched(200);
+    check_cpu_delta(60);
     if (failures) {
         std::fprintf(stderr, "%d checks failed\n", failures);
         return 1;

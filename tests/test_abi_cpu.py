@@ -35,10 +35,19 @@ def sched_header_functions():
     return sorted(set(re.findall(r"^\s*(?:int|double)\s+(lora_\w+)\s*\(", text, flags=re.M)))
 
 
+def cold_header_functions():
+    with open(os.path.join(ROOT, "include", "lora_coldstart.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|double)\s+(lora_\w+)\s*\(", text, flags=re.M)))
+
+
 def test_header_and_binding_agree():
     assert header_functions() == sorted(L.EXPORTS)
     from paper_2401_11240_amd import sched as SC
     assert sched_header_functions() == sorted(SC.EXPORTS)
+    from paper_2401_11240_amd import coldstart as CS
+    assert cold_header_functions() == sorted(CS.EXPORTS)
 
 
 def test_library_exports_every_declared_symbol():
@@ -50,7 +59,7 @@ def test_library_exports_every_declared_symbol():
     out = subprocess.run(["nm", "-D", "--defined-only", B.lib_path()], capture_output=True,
                          text=True, check=True).stdout
     syms = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
-    for name in header_functions() + sched_header_functions():
+    for name in header_functions() + sched_header_functions() + cold_header_functions():
         assert name in syms, name
 
 

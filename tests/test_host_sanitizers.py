@@ -35,11 +35,12 @@ def test_planner_and_oracle_under_asan_ubsan(tmp_path):
                               f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"] + B.DEVICE_FLAGS + host_san +
                              [src, "-o", objs[-1]], capture_output=True, text=True)
         assert res.returncode == 0, res.stderr[-4000:]
-    # the scheduler: plain C++
-    objs.append(str(tmp_path / "lora_sched.o"))
-    res = subprocess.run([CLANGXX, "-c", "-O1", "-g", "-std=c++17", f"-I{os.path.join(ROOT, 'include')}"] + san +
-                         [os.path.join(CSRC, "lora_sched.cpp"), "-o", objs[-1]], capture_output=True, text=True)
-    assert res.returncode == 0, res.stderr[-4000:]
+    # the scheduler and the CPU LoRA kernel: plain C++
+    for src in ("lora_sched.cpp", "lora_cpu.cpp"):
+        objs.append(str(tmp_path / (src + ".o")))
+        res = subprocess.run([CLANGXX, "-c", "-O1", "-g", "-std=c++17", f"-I{os.path.join(ROOT, 'include')}"] + san +
+                             [os.path.join(CSRC, src), "-o", objs[-1]], capture_output=True, text=True)
+        assert res.returncode == 0, res.stderr[-4000:]
     exe = str(tmp_path / "host_check")
     res = subprocess.run([CLANGXX] + san + objs + ["-L/opt/rocm/lib", "-Wl,-rpath,/opt/rocm/lib", "-lamdhip64",
                                                    "-o", exe], capture_output=True, text=True)
