@@ -75,6 +75,7 @@ def parse():
     ap.add_argument("--base-steps", type=int, default=20)
     ap.add_argument("--costmodel-steps", type=int, default=96,
                     help="decode launches timed per point of the cost-model sweep (0: skip the sweep)")
+    ap.add_argument("--no-coldstart", action="store_true", help="skip the cold-start measurements")
     ap.add_argument("--rotate-mib", type=float, default=640.0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -308,6 +309,131 @@ def measure_base(torch, name, dev, steps, rotate_mib):
     }
 
 
+def measure_coldstart(torch, dev, layers: int = 8, tokens: int = 1024, reps: int = 3):
+    """Cold start (Sections 2.3 C1, 4.1, 4.2) on this GPU and its host:
+    the sync-free hand-off of one layer's x (how long the launching thread is
+    held, against a copy followed by a stream synchronisation); the load of a
+    whole rank-64 adapter of a 7B-class model (32 layers x q, k, v, o at
+    4096 -> 4096: 128 MiB) host -> device on a side stream, and the decode
+    step's latency while it runs; a one-prompt batch of `tokens` tokens whose
+    adapter is cold, over `layers` layers, with the load in flight (CPU
+    assistance), waiting for it (on-demand loading), on the CPU only, and with
+    the adapter resident."""
+    from paper_2401_11240_amd import coldstart as CS
+    from paper_2401_11240_amd import device as D
+    from paper_2401_11240_amd import lora as L
+    from paper_2401_11240_amd import workloads as W
+    out = {}
+    s = torch.cuda.Stream(dev)
+    side = torch.cuda.Stream(dev)
+    flags = CS.HostFlags(2)
+    # hand-off of x [tokens, 4096] bf16
+    h = 4096
+    x = torch.randint(-30000, 30000, (tokens, h), dtype=torch.int16, device=dev)
+    hx = torch.empty((tokens, h), dtype=torch.int16, pin_memory=True)
+    torch.cuda.synchronize()
+    held, lat, native = [], [], []
+    for i in range(20):
+        t0 = time.perf_counter()
+        CS.handoff_x(x, h, tokens, h, hx, h, flags.addr(0), i + 1, s)
+        t1 = time.perf_counter()
+        CS.flag_wait(flags.addr(0), i + 1)
+        t2 = time.perf_counter()
+        held.append(t1 - t0)
+        lat.append(t2 - t0)
+        s.synchronize()
+        t0 = time.perf_counter()
+        with torch.cuda.stream(s):
+            hx.copy_(x, non_blocking=True)
+        s.synchronize()
+        native.append(time.perf_counter() - t0)
+    nb = tokens * h * 2
+    out["handoff"] = {
+        "bytes": nb,
+        "host_held_us": round(1e6 * float(np.median(held)), 2),
+        "signal_seen_us": round(1e6 * float(np.median(lat)), 2),
+        "GBps": round(nb / float(np.median(lat)) / 1e9, 2),
+        "native_copy_and_sync_host_held_us": round(1e6 * float(np.median(native)), 2),
+    }
+    del x, hx
+    # a whole adapter's load on a side stream, and decode steps beside it
+    nbytes = 32 * 4 * 64 * (4096 + 4096) * 2
+    src = torch.empty(nbytes // 2, dtype=torch.int16).pin_memory()
+    dst = torch.empty(nbytes // 2, dtype=torch.int16, device=dev)
+    wd = W.NAMED["decode_mixed"]()
+    dw = D.upload(wd, dev)
+    p = dw.projections[0]
+    plan = L.lora_plan_create(p.table, dw.batch, s)
+    xd = dw.xs[p.x]
+    n_dec = 200
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        L.lora_plan_apply(plan, p.table, xd, xd.shape[1], p.y, p.y.shape[1], s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        for _ in range(n_dec):
+            L.lora_plan_apply(plan, p.table, xd, xd.shape[1], p.y, p.y.shape[1], s)
+    with torch.cuda.stream(s):
+        g.replay()
+    torch.cuda.synchronize()
+
+    def decode_us():
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            e0.record(s)
+            g.replay()
+            e1.record(s)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n_dec
+
+    alone = [decode_us() for _ in range(3)]
+    loads, beside = [], []
+    seq = 100
+    for _ in range(3):
+        seq += 1
+        t0 = time.perf_counter()
+        CS.adapter_load_async(dst, src, nbytes, flags.addr(1), seq, side)
+        beside.append(decode_us())
+        CS.flag_wait(flags.addr(1), seq)
+        loads.append(time.perf_counter() - t0)
+        torch.cuda.synchronize()
+    L.lora_plan_status(plan, s)
+    L.lora_plan_destroy(plan)
+    dw.release()
+    del g
+    out["adapter_load"] = {
+        "bytes": nbytes,
+        "ms": round(1e3 * float(np.median(loads)), 3),
+        "GBps": round(nbytes / float(np.median(loads)) / 1e9, 2),
+        "decode_step_us_alone": round(float(np.median(alone)), 3),
+        "decode_step_us_during_load": round(float(np.median(beside)), 3),
+    }
+    # the cold prompt over `layers` layers
+    ws = [W.build_workload(name=f"cold_prompt_l{i}", seed=200 + i, dtype=W.BF16, n_adapters=1, fixed_ranks=[64],
+                           seg_adapter=[0], seg_lens=[tokens], projections=(("q_proj", 4096, 4096, "x"),),
+                           base_weight=True) for i in range(layers)]
+    P = CS.ColdStartPrompt(torch, ws, cold=0, dev=dev, max_threads=16)
+    rest = nbytes - layers * 64 * (4096 + 4096) * 2
+    ballast = (src[: rest // 2], dst[: rest // 2])
+    res = {}
+    for mode in ("gpu", "wait", "assist", "cpu"):
+        ms, paths = [], None
+        for _ in range(reps):
+            r = P.run(s, mode=mode, side_stream=side, ballast=ballast)
+            ms.append(r.ms)
+            paths = r.paths
+        res[mode] = {"ms": round(float(np.median(ms)), 3), "layers_on_cpu": paths.count("cpu")}
+    P.release()
+    flags.free()
+    out["cold_prompt"] = {"tokens": tokens, "layers": layers, "rank": 64, "h": 4096, "dtype": "bf16",
+                          "load_bytes": nbytes, "cpu_threads": 16, **res}
+    del src, dst
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def sources_hash() -> str:
     import hashlib
     csrc = os.path.join(ROOT, "paper_2401_11240_amd", "csrc")
@@ -502,6 +628,9 @@ def main():
             "points": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in p.items()} for p in pts],
             "simulation": sims,
         }
+    if not args.no_coldstart:
+        log("[coldstart] hand-off, adapter load, cold prompt")
+        out["coldstart"] = measure_coldstart(torch, dev)
     if args.calibrate_copy_mib > 0:
         n = int(args.calibrate_copy_mib * 2 ** 20)
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)

@@ -6,6 +6,7 @@
 #include <immintrin.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 #include <string>
@@ -53,23 +54,102 @@ struct Job {
     int64_t ld_delta;
 };
 
-// rows [t0, t1): v = x[t] . A (rank floats), then delta[t] = sum_j (s v_j) B[j]
-void run_rows(const Job& J, int32_t t0, int32_t t1) {
-    std::vector<float> xr(J.h_in), v(J.rank);
-    for (int32_t t = t0; t < t1; ++t) {
-        widen(J.x + (int64_t)t * J.ldx, xr.data(), J.h_in, J.dtype);
-        std::fill(v.begin(), v.end(), 0.f);
-        for (int32_t k = 0; k < J.h_in; ++k) {
-            const float xk = xr[k];
-            const float* a = J.A + (int64_t)k * J.rank;
-            for (int32_t j = 0; j < J.rank; ++j) v[j] += xk * a[j];
+constexpr int32_t kKChunk = 128;   // rows of A kept in L1 while every row of a slice runs over them
+
+// C[i][0..16) (+)= sum_k X_i[k] Y[k][0..16) for four rows X_0..X_3: a 4 x 16
+// register tile of eight 8-wide accumulators, each sum taken in k order with
+// fused multiply-adds, started from C (ACC) or from zero
+template <bool ACC>
+inline void tile4x16(const float* const X[4], const float* Y, int64_t ldy, int32_t K, float* const C[4]) {
+    __m256 c00, c01, c10, c11, c20, c21, c30, c31;
+    if (ACC) {
+        c00 = _mm256_loadu_ps(C[0]), c01 = _mm256_loadu_ps(C[0] + 8), c10 = _mm256_loadu_ps(C[1]);
+        c11 = _mm256_loadu_ps(C[1] + 8), c20 = _mm256_loadu_ps(C[2]), c21 = _mm256_loadu_ps(C[2] + 8);
+        c30 = _mm256_loadu_ps(C[3]), c31 = _mm256_loadu_ps(C[3] + 8);
+    } else {
+        c00 = c01 = c10 = c11 = c20 = c21 = c30 = c31 = _mm256_setzero_ps();
+    }
+    for (int32_t k = 0; k < K; ++k) {
+        const float* y = Y + (int64_t)k * ldy;
+        const __m256 y0 = _mm256_loadu_ps(y), y1 = _mm256_loadu_ps(y + 8);
+        __m256 b = _mm256_broadcast_ss(X[0] + k);
+        c00 = _mm256_fmadd_ps(b, y0, c00);
+        c01 = _mm256_fmadd_ps(b, y1, c01);
+        b = _mm256_broadcast_ss(X[1] + k);
+        c10 = _mm256_fmadd_ps(b, y0, c10);
+        c11 = _mm256_fmadd_ps(b, y1, c11);
+        b = _mm256_broadcast_ss(X[2] + k);
+        c20 = _mm256_fmadd_ps(b, y0, c20);
+        c21 = _mm256_fmadd_ps(b, y1, c21);
+        b = _mm256_broadcast_ss(X[3] + k);
+        c30 = _mm256_fmadd_ps(b, y0, c30);
+        c31 = _mm256_fmadd_ps(b, y1, c31);
+    }
+    _mm256_storeu_ps(C[0], c00);
+    _mm256_storeu_ps(C[0] + 8, c01);
+    _mm256_storeu_ps(C[1], c10);
+    _mm256_storeu_ps(C[1] + 8, c11);
+    _mm256_storeu_ps(C[2], c20);
+    _mm256_storeu_ps(C[2] + 8, c21);
+    _mm256_storeu_ps(C[3], c30);
+    _mm256_storeu_ps(C[3] + 8, c31);
+}
+
+// C[i][0..N) (+)= X_i . Y over k in [0, K) for the rows of a block (nt <= 4;
+// missing rows repeat the last one and are not stored); columns past the
+// last whole 16 one at a time, in the same k order
+template <bool ACC>
+void block_product(const float* const X[4], int nt, const float* Y, int64_t ldy, int32_t K, int32_t N,
+                   float* const C[4]) {
+    float scratch[4][16];
+    int32_t n = 0;
+    for (; n + 16 <= N; n += 16) {
+        float* dst[4];
+        for (int i = 0; i < 4; ++i) {
+            dst[i] = i < nt ? C[i] + n : scratch[i];
+            if (ACC && i >= nt) std::memcpy(scratch[i], C[nt - 1] + n, sizeof scratch[i]);
         }
-        float* out = J.delta + (int64_t)t * J.ld_delta;
-        std::fill(out, out + J.h_out, 0.f);
-        for (int32_t j = 0; j < J.rank; ++j) {
-            const float sv = J.scale * v[j];
-            const float* b = J.B + (int64_t)j * J.h_out;
-            for (int32_t n = 0; n < J.h_out; ++n) out[n] += sv * b[n];
+        tile4x16<ACC>(X, Y + n, ldy, K, dst);
+    }
+    for (; n < N; ++n)
+        for (int i = 0; i < nt; ++i) {
+            float c = ACC ? C[i][n] : 0.f;
+            for (int32_t k = 0; k < K; ++k) c = std::fma(X[i][k], Y[(int64_t)k * ldy + n], c);
+            C[i][n] = c;
+        }
+}
+
+// rows [t0, t1): v = x[t] . A over chunks of kKChunk rows of A (every row of
+// the slice runs over a chunk while it is in L1), then delta[t] = (s v) . B
+// one 16-column block of B at a time (the block stays in L1 across the rows)
+void run_rows(const Job& J, int32_t t0, int32_t t1) {
+    const int32_t R = J.rank, n = t1 - t0;
+    std::vector<float> xr((size_t)n * J.h_in), v((size_t)n * R, 0.f);
+    for (int32_t i = 0; i < n; ++i) widen(J.x + (int64_t)(t0 + i) * J.ldx, xr.data() + (size_t)i * J.h_in, J.h_in, J.dtype);
+    auto rows = [&](int32_t tb, int nt, const float* base, size_t ld, int64_t off, const float* P[4]) {
+        for (int i = 0; i < 4; ++i) P[i] = base + (size_t)(tb + std::min(i, nt - 1)) * ld + off;
+    };
+    for (int32_t k0 = 0; k0 < J.h_in; k0 += kKChunk) {
+        const int32_t kc = std::min(kKChunk, J.h_in - k0);
+        for (int32_t tb = 0; tb < n; tb += 4) {
+            const int nt = std::min<int32_t>(4, n - tb);
+            const float* X[4];
+            rows(tb, nt, xr.data(), J.h_in, k0, X);
+            float* V[4];
+            for (int i = 0; i < 4; ++i) V[i] = v.data() + (size_t)(tb + std::min(i, nt - 1)) * R;
+            block_product<true>(X, nt, J.A + (int64_t)k0 * R, R, kc, R, V);
+        }
+    }
+    for (float& e : v) e *= J.scale;
+    for (int32_t n0 = 0; n0 < J.h_out; n0 += 16) {
+        const int32_t nc = std::min<int32_t>(16, J.h_out - n0);
+        for (int32_t tb = 0; tb < n; tb += 4) {
+            const int nt = std::min<int32_t>(4, n - tb);
+            const float* Vr[4];
+            rows(tb, nt, v.data(), R, 0, Vr);
+            float* O[4];
+            for (int i = 0; i < 4; ++i) O[i] = J.delta + (int64_t)(t0 + tb + std::min(i, nt - 1)) * J.ld_delta + n0;
+            block_product<false>(Vr, nt, J.B + n0, J.h_out, R, nc, O);
         }
     }
 }
