@@ -409,25 +409,31 @@ def measure_coldstart(torch, dev, layers: int = 8, tokens: int = 1024, reps: int
         "decode_step_us_alone": round(float(np.median(alone)), 3),
         "decode_step_us_during_load": round(float(np.median(beside)), 3),
     }
-    # the cold prompt over `layers` layers
-    ws = [W.build_workload(name=f"cold_prompt_l{i}", seed=200 + i, dtype=W.BF16, n_adapters=1, fixed_ranks=[64],
-                           seg_adapter=[0], seg_lens=[tokens], projections=(("q_proj", 4096, 4096, "x"),),
-                           base_weight=True) for i in range(layers)]
-    P = CS.ColdStartPrompt(torch, ws, cold=0, dev=dev, max_threads=16)
+    # a cold prompt over `layers` layers, at two prompt lengths
     rest = nbytes - layers * 64 * (4096 + 4096) * 2
     ballast = (src[: rest // 2], dst[: rest // 2])
-    res = {}
-    for mode in ("gpu", "wait", "assist", "cpu"):
-        ms, paths = [], None
-        for _ in range(reps):
-            r = P.run(s, mode=mode, side_stream=side, ballast=ballast)
-            ms.append(r.ms)
-            paths = r.paths
-        res[mode] = {"ms": round(float(np.median(ms)), 3), "layers_on_cpu": paths.count("cpu")}
-    P.release()
+    out["cold_prompt"] = {}
+    for toks in (tokens, 128):
+        ws = [W.build_workload(name=f"cold_prompt_l{i}", seed=200 + i, dtype=W.BF16, n_adapters=1,
+                               fixed_ranks=[64], seg_adapter=[0], seg_lens=[toks],
+                               projections=(("q_proj", 4096, 4096, "x"),), base_weight=True) for i in range(layers)]
+        P = CS.ColdStartPrompt(torch, ws, cold=0, dev=dev, max_threads=16)
+        res = {}
+        for mode in ("gpu", "wait", "assist", "cpu", "assist_profiled"):
+            ms, paths = [], None
+            kw = {}
+            if mode == "assist_profiled":
+                # the profile: the CPU path's time per layer and the load's rate, both measured above
+                kw = dict(cpu_layer_ms=res["cpu"]["ms"] / layers, load_gbps=out["adapter_load"]["GBps"])
+            for _ in range(reps):
+                r = P.run(s, mode=mode.split("_")[0], side_stream=side, ballast=ballast, **kw)
+                ms.append(r.ms)
+                paths = r.paths
+            res[mode] = {"ms": round(float(np.median(ms)), 3), "layers_on_cpu": paths.count("cpu")}
+        P.release()
+        out["cold_prompt"][f"tokens_{toks}"] = {"tokens": toks, "layers": layers, "rank": 64, "h": 4096,
+                                                "dtype": "bf16", "load_bytes": nbytes, "cpu_threads": 16, **res}
     flags.free()
-    out["cold_prompt"] = {"tokens": tokens, "layers": layers, "rank": 64, "h": 4096, "dtype": "bf16",
-                          "load_bytes": nbytes, "cpu_threads": 16, **res}
     del src, dst
     torch.cuda.synchronize()
     torch.cuda.empty_cache()

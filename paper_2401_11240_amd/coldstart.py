@@ -210,8 +210,11 @@ class ColdStartPrompt:
         (a pinned host tensor, a device tensor of the same bytes) is copied
         first: the rest of a whole adapter (the layers and projections this
         prompt does not run), so that the load takes as long as a real one."""
+        self.load_bytes = sum(L_.cold_A_host.numel() * 2 + L_.cold_B_host.numel() * 2 for L_ in self.layers)
+        self.load_started = time.perf_counter()
         if ballast is not None:
             src, dst = ballast
+            self.load_bytes += src.numel() * src.element_size()
             self.seq_load += 1
             adapter_load_async(dst, src, src.numel() * src.element_size(), self.flags.addr(0), self.seq_load,
                                side_stream)
@@ -227,10 +230,17 @@ class ColdStartPrompt:
         self.load_event = ev
         return self.seq_load
 
-    def run(self, stream, mode: str = "assist", side_stream=None, ballast=None) -> PromptResult:
+    def run(self, stream, mode: str = "assist", side_stream=None, ballast=None, cpu_layer_ms: float = None,
+            load_gbps: float = None) -> PromptResult:
         """mode: "assist" (CPU until the load lands, then GPU), "cpu" (every
         layer on the CPU path), "gpu" (adapter already resident), "wait"
-        (load, wait for it, then every layer on the GPU: on-demand loading)."""
+        (load, wait for it, then every layer on the GPU: on-demand loading).
+
+        With a profile (cpu_layer_ms, the CPU path's time per layer, and
+        load_gbps, the host -> device rate), "assist" starts a CPU layer only
+        while the load's predicted remaining time exceeds it, and otherwise
+        waits for the load: a CPU layer that would end after the adapter lands
+        only delays the GPU's take-over."""
         torch = self.torch
         res = PromptResult()
         t0 = time.perf_counter()
@@ -242,10 +252,17 @@ class ColdStartPrompt:
                 stream.wait_event(self.load_event)
         on_gpu = mode in ("gpu", "wait")
         for li, L_ in enumerate(self.layers):
-            if not on_gpu and mode == "assist" and flag_test(self.flags.addr(0), target):
-                stream.wait_event(self.load_event)       # GPU-side order after the copies
-                on_gpu = True
-                res.load_seen_at_layer = li
+            if not on_gpu and mode == "assist":
+                landed = flag_test(self.flags.addr(0), target)
+                if not landed and cpu_layer_ms and load_gbps:
+                    left_ms = self.load_bytes / (load_gbps * 1e6) - (time.perf_counter() - self.load_started) * 1e3
+                    if left_ms < cpu_layer_ms:
+                        flag_wait(self.flags.addr(0), target)
+                        landed = True
+                if landed:
+                    stream.wait_event(self.load_event)       # GPU-side order after the copies
+                    on_gpu = True
+                    res.load_seen_at_layer = li
             if on_gpu:
                 self._layer_gpu(L_, stream)
                 res.paths.append("gpu")
