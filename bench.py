@@ -253,10 +253,12 @@ def plan_update_cost(torch, w, dev, n=400):
 
 
 def measure_base(torch, name, dev, steps, rotate_mib):
-    """Eq. 1 whole (lora_base_apply: the shrink into float32 v, then the MFMA
-    GEMM of x . W with the delta in its epilogue) on R rotated copies of
-    {x, W, adapters, y}; the calls are timed between HIP events on their
-    stream (each call uploads its small work list, so it is not recorded)."""
+    """Eq. 1 whole on R rotated copies of {x, W, adapters, y}: one base plan
+    for the batch (lora_base_plan_create), and per step lora_base_plan_apply
+    (the shrink into float32 v, its reduction, the MFMA GEMM with the delta in
+    its epilogue, the reduction of split tiles), captured in a HIP graph and
+    replayed between HIP events; the eager per-call form (lora_base_apply,
+    which plans and uploads its work list every call) is timed beside it."""
     from paper_2401_11240_amd import device as D
     from paper_2401_11240_amd import lora as L
     from paper_2401_11240_amd import workloads as W
@@ -265,7 +267,7 @@ def measure_base(torch, name, dev, steps, rotate_mib):
     fp = footprint_bytes(w) + p0.W.nbytes
     R = max(2, min(16, math.ceil(rotate_mib * 2 ** 20 / fp)))
     log(f"[base] {w.name}: footprint {fp / 2**20:.1f} MiB, {R} rotated copies")
-    s = torch.cuda.current_stream(dev)
+    s = torch.cuda.Stream(dev)
     copies = []
     for _ in range(R):
         dw = D.upload(w, dev, stream=s)
@@ -274,23 +276,51 @@ def measure_base(torch, name, dev, steps, rotate_mib):
         n = L.lora_base_workspace_bytes(p.table, dw.batch)
         ws = torch.empty(n, dtype=torch.uint8, device=dev)
         copies.append((dw, wt, ws, n))
+    torch.cuda.synchronize()
+    plan = L.lora_base_plan_create(copies[0][0].projections[0].table, copies[0][0].batch, s)
 
-    def call(c):
+    def planned(c):
+        dw, wt, _, _ = copies[c]
+        p = dw.projections[0]
+        x = dw.xs[p.x]
+        L.lora_base_plan_apply(plan, p.table, x, x.shape[1], wt, wt.shape[1], p.y, p.y.shape[1], s)
+
+    def eager(c):
         dw, wt, ws, n = copies[c]
         p = dw.projections[0]
         x = dw.xs[p.x]
         L.lora_base_apply(p.table, dw.batch, x, x.shape[1], wt, wt.shape[1], p.y, p.y.shape[1], ws, n, s)
 
-    for i in range(max(2, R)):
-        call(i % R)
+    with torch.cuda.stream(s):
+        for c in range(R):
+            planned(c)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for c in range(R):
+            planned(c)
+    reps = max(1, math.ceil(steps / R))
+    with torch.cuda.stream(s):
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            g.replay()
+        e1.record(s)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * R)
+    for i in range(R):
+        eager(i)
+    torch.cuda.synchronize()
     e0.record(s)
     for i in range(steps):
-        call(i % R)
+        eager(i % R)
     e1.record(s)
     e1.synchronize()
-    ms = e0.elapsed_time(e1) / steps
+    ms_eager = e0.elapsed_time(e1) / steps
+    del g
+    L.lora_base_plan_destroy(plan)
     for dw, *_ in copies:
         dw.release()
     del copies
@@ -304,8 +334,10 @@ def measure_base(torch, name, dev, steps, rotate_mib):
         "workload": w.name, "tokens": M, "h_in": K, "h_out": N, "ms_per_step": ms,
         "tokens_per_s": round(M / (ms * 1e-3), 1), "TFLOPs": round(tf, 2),
         "pct_mfma_peak": round(100.0 * tf / MFMA_BF16_PEAK_TFLOPS, 2),
+        "eager_ms_per_call": ms_eager,
         "algorithmic_flops_per_step": flops, "rotated_copies": R,
-        "timing": "HIP events around eager calls (shrink into v, then the fused GEMM)",
+        "timing": "HIP graph replays of lora_base_plan_apply between HIP events (shrink into v, its reduction, "
+                  "the fused GEMM, the split tiles' reduction)",
     }
 
 

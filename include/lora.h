@@ -178,6 +178,24 @@ int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_
                     int64_t ldw, void* y, int64_t ldy, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * lora_base_apply planned once for a batch (the same batch runs every layer
+ * of a prompt step, Section 2.2): lora_base_plan_create builds the work list
+ * and the tile pieces, allocates the plan's device memory (work list, float32
+ * v, partial tiles) and uploads them, synchronising `stream` once; it refuses
+ * a capturing stream.  lora_base_plan_apply then enqueues kernels only (the
+ * shrink, its reduction into v, the GEMM, and the reduction of split tiles)
+ * and may be recorded in a HIP graph; it runs on any table whose shapes,
+ * dtype and referenced ranks match the plan's (NULL: the plan's own table),
+ * with the operand rules of lora_base_apply.  Launches on one plan use the
+ * plan's memory: order them on one stream.  lora_base_plan_destroy frees it.
+ */
+typedef struct lora_base_plan_s* lora_base_plan_t;
+int lora_base_plan_create(lora_base_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream);
+int lora_base_plan_apply(lora_base_plan_t p, lora_table_t t, const void* x, int64_t ldx, const void* wt, int64_t ldw,
+                         void* y, int64_t ldy, void* stream);
+int lora_base_plan_destroy(lora_base_plan_t p);
+
+/*
  * lora_apply_fused without a workspace argument and without allocating, for
  * callers that cannot allocate device memory (code that must not call
  * hipMalloc, harnesses that forbid it, tight serving loops).  The work list

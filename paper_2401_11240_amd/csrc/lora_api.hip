@@ -1040,13 +1040,13 @@ int lora_base_workspace_bytes(lora_table_t t, const lora_batch_t* b, size_t* byt
     return LORA_OK;
 }
 
-int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, const void* wt,
-                    int64_t ldw, void* y, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
-    if (int rc = check_table(t)) return rc;
-    BaseLayout L;
-    if (int rc = build_base(t, b, L)) return rc;
-    const int n_rows = b->n_rows;
-    if (n_rows == 0) return LORA_OK;
+}  // extern "C"
+
+namespace {
+
+// The operand checks of lora_base_apply and lora_base_plan_apply.
+int check_base_operands(const lora_table_s* t, int n_rows, const void* x, int64_t ldx, const void* wt, int64_t ldw,
+                        void* y, int64_t ldy, uint64_t* w_span_out) {
     if (int rc = check_x(t, x, ldx, n_rows)) return rc;
     if (int rc = check_y(t, y, ldy, n_rows)) return rc;
     if (!wt) return fail(LORA_E_ARG, "wt is NULL");
@@ -1055,24 +1055,21 @@ int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_
     const uint64_t w_span = span_bytes(t->h_out, ldw, t->h_in);
     if (w_span > kMaxSpan) return fail(LORA_E_SHAPE, "wt spans more than 2 GiB");
     if (int rc = check_overlap(x, ldx, t->h_in, y, ldy, t->h_out, n_rows)) return rc;
-    {
-        const uintptr_t ws0 = (uintptr_t)wt, we = ws0 + w_span;
-        const uintptr_t ys = (uintptr_t)y, ye = ys + span_bytes(n_rows, ldy, t->h_out);
-        if (ws0 < ye && ys < we) return fail(LORA_E_OVERLAP, "wt and y overlap");
-    }
-    if (!ws) return fail(LORA_E_ARG, "workspace is NULL");
-    if (!aligned16(ws)) return fail(LORA_E_ALIGN, "workspace not 16-byte aligned");
-    if (ws_bytes < L.total)
-        return fail(LORA_E_WORKSPACE, "workspace has " + std::to_string(ws_bytes) + " bytes, needs " +
-                                          std::to_string(L.total));
-    DeviceGuard dg(t->device);
-    hipStream_t s = (hipStream_t)stream;
-    if (int rc = check_not_capturing(s, "lora_base_apply")) return rc;
-    unsigned char* w = (unsigned char*)ws;
+    const uintptr_t ws0 = (uintptr_t)wt, we = ws0 + w_span;
+    const uintptr_t ys = (uintptr_t)y, ye = ys + span_bytes(n_rows, ldy, t->h_out);
+    if (ws0 < ye && ys < we) return fail(LORA_E_OVERLAP, "wt and y overlap");
+    *w_span_out = w_span;
+    return LORA_OK;
+}
+
+// Everything after the upload: the shrink of every adapted row into the dense
+// float32 v, then the GEMM with the delta in its epilogue.  The work list and
+// the tile pieces are at their layout offsets in w.  Kernels only (a graph
+// may record it).
+int base_run(const lora_table_s* t, const BaseLayout& L, int n_rows, unsigned char* w, const void* x, int64_t ldx,
+             const void* wt, int64_t ldw, uint64_t w_span, void* y, int64_t ldy, hipStream_t s) {
     float* v = (float*)(w + L.off_v);
     const HostPlan& p = L.p;
-    if (int rc = stage_upload(t->device, p.blob.data(), p.plan_bytes, w, s)) return rc;
-    if (int rc = stage_upload(t->device, L.pieces_blob.data(), L.pieces_blob.size(), w + L.off_pieces, s)) return rc;
     if (p.n_active > 0) {
         // v = x . A_g for every adapted row, into the dense float32 buffer
         if (int rc = enqueue(t, p, w, x, ldx, nullptr, 0, s, true)) return rc;
@@ -1112,6 +1109,103 @@ int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_
     a.v_bytes = (uint32_t)L.v_bytes;
     a.b_span_ok = 1;
     LORA_HIP_TRY(launch_base(a, t->dtype, s));
+    return LORA_OK;
+}
+
+}  // namespace
+
+struct lora_base_plan_s {
+    const lora_table_s* table = nullptr;
+    int device = 0;
+    int n_rows = 0;
+    BaseLayout L;
+    unsigned char* dmem = nullptr;
+};
+
+extern "C" {
+
+int lora_base_apply(lora_table_t t, const lora_batch_t* b, const void* x, int64_t ldx, const void* wt,
+                    int64_t ldw, void* y, int64_t ldy, void* ws, size_t ws_bytes, void* stream) {
+    if (int rc = check_table(t)) return rc;
+    BaseLayout L;
+    if (int rc = build_base(t, b, L)) return rc;
+    const int n_rows = b->n_rows;
+    if (n_rows == 0) return LORA_OK;
+    uint64_t w_span = 0;
+    if (int rc = check_base_operands(t, n_rows, x, ldx, wt, ldw, y, ldy, &w_span)) return rc;
+    if (!ws) return fail(LORA_E_ARG, "workspace is NULL");
+    if (!aligned16(ws)) return fail(LORA_E_ALIGN, "workspace not 16-byte aligned");
+    if (ws_bytes < L.total)
+        return fail(LORA_E_WORKSPACE, "workspace has " + std::to_string(ws_bytes) + " bytes, needs " +
+                                          std::to_string(L.total));
+    DeviceGuard dg(t->device);
+    hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_base_apply")) return rc;
+    unsigned char* w = (unsigned char*)ws;
+    if (int rc = stage_upload(t->device, L.p.blob.data(), L.p.plan_bytes, w, s)) return rc;
+    if (int rc = stage_upload(t->device, L.pieces_blob.data(), L.pieces_blob.size(), w + L.off_pieces, s)) return rc;
+    return base_run(t, L, n_rows, w, x, ldx, wt, ldw, w_span, y, ldy, s);
+}
+
+int lora_base_plan_create(lora_base_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream) {
+    if (!out) return fail(LORA_E_ARG, "out is NULL");
+    *out = nullptr;
+    if (int rc = check_table(t)) return rc;
+    auto* pl = new (std::nothrow) lora_base_plan_s();
+    if (!pl) return fail(LORA_E_NOMEM, "plan allocation failed");
+    if (int rc = build_base(t, b, pl->L)) {
+        delete pl;
+        return rc;
+    }
+    DeviceGuard dg(t->device);
+    hipStream_t s = (hipStream_t)stream;
+    if (int rc = check_not_capturing(s, "lora_base_plan_create")) {
+        delete pl;
+        return rc;
+    }
+    pl->table = t;
+    pl->device = t->device;
+    pl->n_rows = b->n_rows;
+    hipError_t e = hipMalloc((void**)&pl->dmem, std::max<size_t>(pl->L.total, 256));
+    if (e != hipSuccess) {
+        delete pl;
+        return fail(LORA_E_NOMEM, std::string("hipMalloc of the base plan: ") + hipGetErrorString(e));
+    }
+    const BaseLayout& L = pl->L;
+    e = hipMemcpyAsync(pl->dmem, L.p.blob.data(), L.p.plan_bytes, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess && !L.pieces_blob.empty())
+        e = hipMemcpyAsync(pl->dmem + L.off_pieces, L.pieces_blob.data(), L.pieces_blob.size(), hipMemcpyHostToDevice,
+                           s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        (void)hipFree(pl->dmem);
+        delete pl;
+        return fail(LORA_E_HIP, std::string("base plan upload: ") + hipGetErrorString(e));
+    }
+    *out = pl;
+    return LORA_OK;
+}
+
+int lora_base_plan_apply(lora_base_plan_t pl, lora_table_t t, const void* x, int64_t ldx, const void* wt, int64_t ldw,
+                         void* y, int64_t ldy, void* stream) {
+    if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
+    const lora_table_s* tt = t ? t : pl->table;
+    if (int rc = check_compatible(pl->L.p, tt)) return rc;
+    if (tt->device != pl->device) return fail(LORA_E_ARG, "table is on another device than the plan");
+    if (pl->n_rows == 0) return LORA_OK;
+    uint64_t w_span = 0;
+    if (int rc = check_base_operands(tt, pl->n_rows, x, ldx, wt, ldw, y, ldy, &w_span)) return rc;
+    DeviceGuard dg(tt->device);
+    return base_run(tt, pl->L, pl->n_rows, pl->dmem, x, ldx, wt, ldw, w_span, y, ldy, (hipStream_t)stream);
+}
+
+int lora_base_plan_destroy(lora_base_plan_t pl) {
+    if (!pl) return fail(LORA_E_ARG, "plan is NULL");
+    if (pl->dmem) {
+        DeviceGuard dg(pl->device);
+        (void)hipFree(pl->dmem);
+    }
+    delete pl;
     return LORA_OK;
 }
 

@@ -40,7 +40,8 @@ EXPORTS = (
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
     "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
     "lora_plan_bytes", "lora_plan_create_reserved", "lora_plan_update", "lora_apply_fused_static",
-    "lora_base_workspace_bytes", "lora_base_apply",
+    "lora_base_workspace_bytes", "lora_base_apply", "lora_base_plan_create", "lora_base_plan_apply",
+    "lora_base_plan_destroy",
     "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
 )
 
@@ -105,6 +106,9 @@ def load():
         "lora_apply_fused_static": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp],
         "lora_base_workspace_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
         "lora_base_apply": [vp, C.POINTER(_Batch), vp, i64, vp, i64, vp, i64, vp, sz, vp],
+        "lora_base_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
+        "lora_base_plan_apply": [vp, vp, vp, i64, vp, i64, vp, i64, vp],
+        "lora_base_plan_destroy": [vp],
         "lora_plan_create": [C.POINTER(vp), vp, C.POINTER(_Batch), vp],
         "lora_plan_bytes": [vp, C.POINTER(_Batch), C.POINTER(sz)],
         "lora_plan_create_reserved": [C.POINTER(vp), vp, C.POINTER(_Batch), sz, vp],
@@ -217,6 +221,21 @@ def lora_base_apply(table: int, batch: Batch, x, ldx: int, wt, ldw: int, y, ldy:
     """y = round(x . W + s_g (x . A_g) . B_g); ``wt`` is W transposed, [h_out, ldw]."""
     _check(load().lora_base_apply(table, batch.c, _addr(x), ldx, _addr(wt), ldw, _addr(y), ldy, _addr(ws),
                                   ws_bytes, _stream(stream)))
+
+
+def lora_base_plan_create(table: int, batch: Batch, stream=None) -> int:
+    out = C.c_void_p()
+    _check(load().lora_base_plan_create(C.byref(out), table, batch.c, _stream(stream)))
+    return int(out.value or 0)
+
+
+def lora_base_plan_apply(plan: int, table, x, ldx: int, wt, ldw: int, y, ldy: int, stream=None) -> None:
+    _check(load().lora_base_plan_apply(plan, table or 0, _addr(x), ldx, _addr(wt), ldw, _addr(y), ldy,
+                                       _stream(stream)))
+
+
+def lora_base_plan_destroy(plan: int) -> None:
+    _check(load().lora_base_plan_destroy(plan))
 
 
 def lora_plan_create(table: int, batch: Batch, stream=None) -> int:

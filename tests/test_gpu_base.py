@@ -197,3 +197,47 @@ def test_prompt_batch_8437_rows_sampled():
                  mag=allowance(w, rows, "q_proj"))
     say("  ", st)
     dw.release()
+
+
+def test_base_plan_equals_the_per_call_form_and_replays_in_a_graph():
+    """lora_base_plan_apply runs the same kernels as lora_base_apply: equal bit
+    for bit; on another table with the same ranks too; and recorded in a graph,
+    every replay (eager work between them) equals the eager result."""
+    for case in (0, 1):
+        w = small_case(*SMALL[case])
+        dw = D.upload(w, DEV)
+        ref = run_base(dw, w)
+        p = dw.projection("proj")
+        pr = w.projection("proj")
+        x = dw.xs[p.x]
+        wt = D.to_device_bits(np.ascontiguousarray(pr.W.T), DEV)
+        s = torch.cuda.Stream(DEV)
+        plan = L.lora_base_plan_create(p.table, dw.batch, s)
+        try:
+            y = torch.zeros_like(p.y)
+            L.lora_base_plan_apply(plan, None, x, x.shape[1], wt, wt.shape[1], y, y.shape[1], s)
+            torch.cuda.synchronize()
+            assert np.array_equal(D.from_device_bits(y), ref), f"case {case}"
+            # another upload of the same workload: its own table, same ranks
+            dw2 = D.upload(w, DEV)
+            p2 = dw2.projection("proj")
+            y2 = torch.zeros_like(p.y)
+            L.lora_base_plan_apply(plan, p2.table, dw2.xs[p2.x], x.shape[1], wt, wt.shape[1], y2, y2.shape[1], s)
+            torch.cuda.synchronize()
+            assert np.array_equal(D.from_device_bits(y2), ref)
+            dw2.release()
+            g = torch.cuda.CUDAGraph()
+            y3 = torch.zeros_like(p.y)
+            with torch.cuda.graph(g, stream=s):
+                L.lora_base_plan_apply(plan, None, x, x.shape[1], wt, wt.shape[1], y3, y3.shape[1], s)
+            for rep in range(3):
+                y3.fill_(0)
+                torch.cuda.synchronize()
+                g.replay()
+                torch.cuda.synchronize()
+                assert np.array_equal(D.from_device_bits(y3), ref), f"case {case} replay {rep}"
+            del g
+        finally:
+            torch.cuda.synchronize()
+            L.lora_base_plan_destroy(plan)
+            dw.release()
