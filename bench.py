@@ -42,13 +42,13 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, datasheet
 # HBM traffic of one step launch of the headline workload, from two rocprofv3
 # --pmc passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) scaled by the
 # same counters on a plain 256 MiB device copy in the same run (FETCH_SIZE
-# reads 131,092.0 KiB for 262,144 KiB read: x 1.99969; WRITE_SIZE reads
+# reads 131,088.8 KiB for 262,144 KiB read: x 1.99980; WRITE_SIZE reads
 # 262,144.0 KiB: x 1.0).  Valid only for the kernel sources it was taken on
 # (hash of csrc/*); reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "sources_sha256_16": "84dfb1fde182e92f",
+    "sources_sha256_16": "b63f0f111467f364",
     "workload": "decode_q4096_t64_mixed_rank_f16",
-    "fetch_kib": 6650.7, "fetch_scale": 262144.0 / 131092.2,
+    "fetch_kib": 6697.5, "fetch_scale": 262144.0 / 131088.8,
     "write_kib": 732.9, "write_scale": 1.0,
 }
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16
@@ -476,7 +476,8 @@ def sources_hash() -> str:
     import hashlib
     csrc = os.path.join(ROOT, "paper_2401_11240_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("lora_api.hip", "lora_internal.h", "lora_kernels.hip", "lora_device.h", "lora_base.hip"):
+    # the sources the step kernel and its planner are built from
+    for f in ("lora_api.hip", "lora_internal.h", "lora_kernels.hip", "lora_device.h"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
