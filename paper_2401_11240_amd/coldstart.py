@@ -6,8 +6,8 @@ factors are copied host -> device on a side stream (lora_adapter_load_async),
 and until the copy's signal shows up, every layer runs the adapter's rows on
 the CPU: the layer input is handed to the host without a host-side stream
 synchronisation (lora_handoff_x, Section 4.2's asynchronous copy and signal),
-the GPU computes the base projection of every row (lora_base_apply, the cold
-rows as rows without an adapter), the host cores compute x A B for the cold
+the GPU computes the base projection of every row (a base plan of the batch
+with the cold rows as rows without an adapter), the host cores compute x A B for the cold
 rows (lora_cpu_delta, token slices over threads) while it runs, and the delta
 is merged into y (lora_add_delta).  Once loaded, the GPU takes the adapter's
 rows over (the fused base projection plus delta).  Marshalling and
@@ -127,8 +127,6 @@ class Layer:
     included, unfilled until loaded) and the base-projection workspace."""
     dw: object
     wt: object
-    ws: object
-    ws_bytes: int
     cold_A_dev: int = 0           # device address of the cold adapter's A in this layer
     cold_B_dev: int = 0
     cold_A_host: object = None    # pinned host copies (the load's source; the CPU path reads them)
@@ -177,9 +175,6 @@ class ColdStartPrompt:
             p = dw.projections[0]
             pr = w.projections[0]
             wt = D.to_device_bits(np.ascontiguousarray(pr.W.T), dev)
-            n = max(_lora.lora_base_workspace_bytes(p.table, dw.batch),
-                    _lora.lora_base_workspace_bytes(p.table, self.batch_cpu), 16)
-            ws = torch.empty(n, dtype=torch.uint8, device=dev)
             A_h = torch.from_numpy(np.ascontiguousarray(pr.A[cold]).view(np.int16).ravel().copy()).pin_memory()
             B_h = torch.from_numpy(np.ascontiguousarray(pr.B[cold]).view(np.int16).ravel().copy()).pin_memory()
             # the device copies start as NaN: the GPU must not read them before the load
@@ -187,19 +182,27 @@ class ColdStartPrompt:
             b_off = (p.B_ptrs[cold] - p.B_buf.data_ptr()) // 2
             p.A_buf[a_off:a_off + A_h.numel()].fill_(nan16)
             p.B_buf[b_off:b_off + B_h.numel()].fill_(nan16)
-            self.layers.append(Layer(dw, wt, ws, n, p.A_ptrs[cold], p.B_ptrs[cold], A_h, B_h))
+            self.layers.append(Layer(dw, wt, p.A_ptrs[cold], p.B_ptrs[cold], A_h, B_h))
         rows = max(1, self.cold_rows[1] - self.cold_rows[0])
         h_in = workloads[0].projections[0].h_in
         h_out = workloads[0].projections[0].h_out
         self.host_x = torch.empty((rows, h_in), **pin)
         self.host_delta = torch.empty((rows, h_out), dtype=torch.float32, pin_memory=True)
         self.dev_delta = torch.empty((rows, h_out), dtype=torch.float32, device=dev)
+        # one base plan per batch form, shared by the layers (same shapes and ranks):
+        # every adapter on the GPU, and the cold adapter's rows as rows without one
+        t0 = self.layers[0].dw.projections[0].table
+        self.plan_gpu = _lora.lora_base_plan_create(t0, self.layers[0].dw.batch)
+        self.plan_cpu = _lora.lora_base_plan_create(t0, self.batch_cpu)
         self.flags = HostFlags(2)          # 0: the adapter load, 1: the hand-offs
         self.seq_x = 0
         self.seq_load = 0
         torch.cuda.synchronize()
 
     def release(self):
+        self.torch.cuda.synchronize()
+        _lora.lora_base_plan_destroy(self.plan_gpu)
+        _lora.lora_base_plan_destroy(self.plan_cpu)
         for L_ in self.layers:
             L_.dw.release()
         self.flags.free()
@@ -276,8 +279,8 @@ class ColdStartPrompt:
     def _layer_gpu(self, L_, stream):
         p = L_.dw.projections[0]
         x = L_.dw.xs[p.x]
-        _lora.lora_base_apply(p.table, L_.dw.batch, x, x.shape[1], L_.wt, L_.wt.shape[1], p.y, p.y.shape[1], L_.ws,
-                              L_.ws_bytes, stream)
+        _lora.lora_base_plan_apply(self.plan_gpu, p.table, x, x.shape[1], L_.wt, L_.wt.shape[1], p.y, p.y.shape[1],
+                                   stream)
 
     def _layer_cpu(self, L_, stream):
         """Stream order per layer: hand-off of the cold rows' x and its signal,
@@ -293,8 +296,7 @@ class ColdStartPrompt:
         self.seq_x += 1
         handoff_x(x.data_ptr() + 2 * lo * h_in, h_in, n, h_in, self.host_x, h_in, self.flags.addr(1), self.seq_x,
                   stream)
-        _lora.lora_base_apply(p.table, self.batch_cpu, x, h_in, L_.wt, L_.wt.shape[1], p.y, h_out, L_.ws, L_.ws_bytes,
-                              stream)
+        _lora.lora_base_plan_apply(self.plan_cpu, p.table, x, h_in, L_.wt, L_.wt.shape[1], p.y, h_out, stream)
         flag_wait(self.flags.addr(1), self.seq_x)
         cpu_delta(self.host_x, h_in, n, h_in, h_out, self.dtype, L_.cold_A_host, L_.cold_B_host, self.rank,
                   self.scale, self.host_delta, h_out, self.tokens_per_thread, self.max_threads)

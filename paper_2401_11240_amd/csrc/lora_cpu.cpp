@@ -6,9 +6,12 @@
 #include <immintrin.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
+#include <condition_variable>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -158,6 +161,98 @@ void run_rows(const Job& J, int32_t t0, int32_t t1) {
 
 #pragma clang attribute pop
 
+namespace {
+
+// Worker threads kept across calls (starting threads costs tens of
+// microseconds each, a fair part of a short prompt's layer).  A call posts its
+// slices; the workers and the calling thread take them in turn; the call
+// returns when every slice is done and no worker is still looking for one, so
+// that the next call may rewrite the job.  Calls run one at a time.  The pool
+// is never destroyed: its threads wait on it until the process ends.
+struct Pool {
+    std::mutex call_mu;                 // one call at a time
+    std::mutex mu;                      // guards everything below but `next`
+    std::condition_variable cv_work, cv_done;
+    std::vector<std::thread> workers;
+    const Job* job = nullptr;
+    int32_t c = 0, n_rows = 0, n_slices = 0;
+    std::atomic<int32_t> next{0};
+    int32_t done = 0;                   // slices finished in this call
+    int32_t active = 0;                 // workers between taking the job and reporting back
+    uint64_t gen = 0;
+
+    // slices until none is left; returns how many this thread ran
+    int32_t drain(const Job& J, int32_t cc, int32_t rows, int32_t slices) {
+        int32_t ran = 0;
+        for (;;) {
+            const int32_t i = next.fetch_add(1);
+            if (i >= slices) return ran;
+            run_rows(J, i * cc, std::min(rows, (i + 1) * cc));
+            ++ran;
+        }
+    }
+
+    void worker() {
+        uint64_t seen = 0;
+        for (;;) {
+            const Job* J;
+            int32_t cc, rows, slices;
+            {
+                std::unique_lock<std::mutex> lk(mu);
+                cv_work.wait(lk, [&] { return gen != seen && job != nullptr; });
+                seen = gen;
+                ++active;
+                J = job;
+                cc = c;
+                rows = n_rows;
+                slices = n_slices;
+            }
+            const int32_t ran = drain(*J, cc, rows, slices);
+            std::lock_guard<std::mutex> lk(mu);
+            done += ran;
+            --active;
+            cv_done.notify_all();
+        }
+    }
+
+    // false when threads cannot be started
+    bool ensure(int n) {
+        try {
+            while ((int)workers.size() < n) workers.emplace_back(&Pool::worker, this);
+        } catch (...) {
+            return false;
+        }
+        return true;
+    }
+
+    void run(const Job& J, int32_t chunk, int32_t rows, int32_t slices) {
+        {
+            std::unique_lock<std::mutex> lk(mu);
+            cv_done.wait(lk, [&] { return active == 0; });
+            job = &J;
+            c = chunk;
+            n_rows = rows;
+            n_slices = slices;
+            next.store(0);
+            done = 0;
+            ++gen;
+        }
+        cv_work.notify_all();
+        const int32_t ran = drain(J, chunk, rows, slices);
+        std::unique_lock<std::mutex> lk(mu);
+        done += ran;
+        cv_done.wait(lk, [&] { return done == n_slices && active == 0; });
+        job = nullptr;
+    }
+};
+
+Pool* pool() {
+    static Pool* p = new Pool();
+    return p;
+}
+
+}  // namespace
+
 extern "C" int lora_cpu_delta(const void* x, int64_t ldx, int32_t n_rows, int32_t h_in, int32_t h_out, int32_t dtype,
                               const void* A, const void* B, int32_t rank, float scale, float* delta, int64_t ld_delta,
                               int32_t tokens_per_thread, int32_t max_threads) {
@@ -182,18 +277,9 @@ extern "C" int lora_cpu_delta(const void* x, int64_t ldx, int32_t n_rows, int32_
         run_rows(J, 0, n_rows);
         return LORA_OK;
     }
-    std::vector<std::thread> pool;
-    pool.reserve(n_thr - 1);
-    try {
-        for (int32_t i = 1; i < n_thr; ++i) {
-            const int32_t t0 = i * c, t1 = std::min(n_rows, t0 + c);
-            if (t0 < t1) pool.emplace_back(run_rows, std::cref(J), t0, t1);
-        }
-    } catch (...) {
-        for (auto& th : pool) th.join();
-        return lora::set_error(LORA_E_NOMEM, "lora_cpu_delta: cannot start threads");
-    }
-    run_rows(J, 0, std::min(n_rows, c));
-    for (auto& th : pool) th.join();
+    Pool* P = pool();
+    std::lock_guard<std::mutex> call(P->call_mu);
+    if (!P->ensure(n_thr - 1)) return lora::set_error(LORA_E_NOMEM, "lora_cpu_delta: cannot start threads");
+    P->run(J, c, n_rows, (n_rows + c - 1) / c);
     return LORA_OK;
 }
