@@ -655,15 +655,20 @@ def main():
         log("[costmodel] decode sweep over batch sizes x rank mixes")
         pts = CM.decode_sweep(torch, dev, steps=args.costmodel_steps)
         fits = CM.fit(pts)
+        log("[costmodel] prompt sweep")
+        ppts = CM.prefill_sweep(torch, dev)
+        pfits = CM.fit_prefill(ppts)
         log("[costmodel] simulating the routing policies")
         sims = {}
         for kind in ("sum_rank", "padded"):
-            pre_m, dec_m = CM.serving_models(fits, kind)
+            pre_m, dec_m = CM.serving_models(fits, kind, prefill_fit=pfits)
             sims[kind] = CM.simulate_policies(pre_m, dec_m)
             sims[kind]["models_ms"] = {"decode": list(dec_m.as_tuple()), "prefill": list(pre_m.as_tuple())}
         out["cost_model"] = {
             "projection": f"{CM.H_IN}->{CM.H_OUT} f16 decode step launch, one adapter per request",
             "fit_us": fits,
+            "prefill_fit_us": pfits,
+            "prefill_points": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in p.items()} for p in ppts],
             "points": [{k: (round(v, 3) if isinstance(v, float) else v) for k, v in p.items()} for p in pts],
             "simulation": sims,
         }

@@ -43,20 +43,26 @@ def sweep_points(batch_sizes: Sequence[int] = BATCH_SIZES, mixes: Sequence[str] 
     return pts
 
 
-def _workload(ranks: Sequence[int], seed: int):
+def _workload(ranks: Sequence[int], seed: int, lens: Sequence[int] = None):
     b = len(ranks)
     return W.build_workload(name=f"sweep_b{b}", seed=seed, dtype=W.F16, n_adapters=b, fixed_ranks=list(ranks),
-                            seg_adapter=list(range(b)), seg_lens=[1] * b,
+                            seg_adapter=list(range(b)), seg_lens=list(lens) if lens else [1] * b,
                             projections=(("q_proj", H_IN, H_OUT, "x"),))
 
 
+# Prompt batches of the prefill sweep: (segments, tokens per segment); every
+# segment its own adapter, ranks cycling 8/16/32/64.
+PREFILL_POINTS = [(s, n) for s in (1, 2, 4, 8, 16) for n in (64, 256, 1024)]
+
+
 def time_decode(torch, ranks: Sequence[int], dev, steps: int = 200, rotate_mib: float = 256.0,
-                max_copies: int = 48, seed: int = 0) -> float:
-    """Microseconds per decode-step launch of one batch (every request its own
-    adapter), from HIP graph replays over rotated copies of adapters, x and y."""
+                max_copies: int = 48, seed: int = 0, lens: Sequence[int] = None) -> float:
+    """Microseconds per step launch of one batch (every request its own
+    adapter; one token each unless `lens` gives the segments' lengths), from
+    HIP graph replays over rotated copies of adapters, x and y."""
     from . import device as D
     from . import lora as L
-    w = _workload(ranks, seed)
+    w = _workload(ranks, seed, lens)
     fp = sum(x.nbytes for x in w.xs.values()) + sum(
         sum(a.nbytes for a in p.A) + sum(b.nbytes for b in p.B) + p.y.nbytes for p in w.projections)
     R = max(2, min(max_copies, math.ceil(rotate_mib * 2 ** 20 / fp)))
@@ -109,6 +115,30 @@ def decode_sweep(torch, dev, points: Sequence[Dict] = None, steps: int = 200) ->
     return out
 
 
+def prefill_sweep(torch, dev, steps: int = 40) -> List[Dict]:
+    """The step launch on prompt batches (PREFILL_POINTS), for the prompt
+    model: microseconds against the batch's tokens and sum of ranks."""
+    out = []
+    for i, (nseg, n) in enumerate(PREFILL_POINTS):
+        ranks = [(8, 16, 32, 64)[j % 4] for j in range(nseg)]
+        us = time_decode(torch, ranks, dev, steps=steps, seed=100 + i, lens=[n] * nseg, max_copies=16)
+        reqs = [(r, n) for r in ranks]
+        out.append(dict(segments=nseg, tokens_per_segment=n, us=us, tokens=S.perf_feature(S.TOKENS, reqs),
+                        sum_rank=S.perf_feature(S.SUM_RANK, reqs)))
+    return out
+
+
+def fit_prefill(points: Sequence[Dict]) -> Dict:
+    """The prompt model (tokens) fitted to the prefill sweep (microseconds),
+    beside the sum-of-ranks form for comparison."""
+    t = [p["us"] for p in points]
+    res = {}
+    for name, kind in (("tokens", S.TOKENS), ("sum_rank", S.SUM_RANK)):
+        m, r2 = S.perf_fit(kind, [p[name] for p in points], t)
+        res[name] = dict(alpha_us=m.alpha, beta_us=m.beta, r2=r2)
+    return res
+
+
 def fit(points: Sequence[Dict]) -> Dict:
     """Both models of Section 5 fitted to the measured points (microseconds)."""
     t = [p["us"] for p in points]
@@ -121,18 +151,22 @@ def fit(points: Sequence[Dict]) -> Dict:
 
 def serving_models(fit_res: Dict, kind: str = "sum_rank", *, layers: int = 32, projections: int = 4,
                    base_decode_ms: float = 2.5, base_prefill_us_per_token: float = 15.0,
-                   lora_prefill_us_per_token: float = 1.0):
+                   lora_prefill_us_per_token: float = 1.0, prefill_fit: Dict = None):
     """Iteration models of a 7B-class model whose every layer runs the fitted
     decode launch on `projections` projections: decode = base + layers *
     projections * (alpha feature(S) + beta), feature of the chosen fit;
-    prompt = tokens times a base plus adapter cost per token.  The base terms
-    are assumptions for the simulation (the paper profiles a whole serving
-    stack); only the adapter term of the decode model is measured here.
-    Milliseconds."""
+    prompt = tokens times a base plus adapter cost per token (the adapter's
+    share from the prompt fit when given).  The base terms are assumptions for
+    the simulation (the paper profiles a whole serving stack); the adapter
+    terms are measured here.  Milliseconds."""
     f = fit_res[kind]
     launches = layers * projections
     dec = S.model(S.SUM_RANK if kind == "sum_rank" else S.PADDED, launches * f["alpha_us"] / 1000.0,
                   base_decode_ms + launches * f["beta_us"] / 1000.0)
+    if prefill_fit is not None:
+        # the adapter's share of a prompt token, measured: the fitted slope per
+        # launch times the launches of a step
+        lora_prefill_us_per_token = launches * prefill_fit["tokens"]["alpha_us"]
     pre = S.model(S.TOKENS, (base_prefill_us_per_token + lora_prefill_us_per_token) / 1000.0, 0.0)
     return pre, dec
 
