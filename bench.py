@@ -98,11 +98,29 @@ class Rotation:
         self.copies = [D.upload(w, dev, stream=stream) for _ in range(copies)]
         first = self.copies[0]
         self.plans = {p.name: L.lora_plan_create(p.table, first.batch, stream) for p in first.projections}
+        # projections that share an input: one plan of all of them, one launch
+        self.groups = {}
+        for i, p in enumerate(first.projections):
+            self.groups.setdefault((p.x, p.h_out), []).append(i)
+        self.multi = {k: L.lora_plan_create_multi([first.projections[i].table for i in ix], first.batch, stream)
+                      for k, ix in self.groups.items() if len(ix) > 1}
 
     def step(self, c, stream, phase="apply"):
-        """One pass of the delta over every projection of copy c."""
+        """One pass of the delta over every projection of copy c ("multi":
+        the projections that share an input in one launch each)."""
         L = self.L
         dw = self.copies[c]
+        if phase == "multi":
+            for key, ix in self.groups.items():
+                ps = [dw.projections[i] for i in ix]
+                x = dw.xs[key[0]]
+                if len(ps) == 1:
+                    p = ps[0]
+                    L.lora_plan_apply(self.plans[p.name], p.table, x, x.shape[1], p.y, p.y.shape[1], stream)
+                else:
+                    L.lora_plan_apply_multi(self.multi[key], [p.table for p in ps], x, x.shape[1],
+                                            [p.y for p in ps], [p.y.shape[1] for p in ps], stream)
+            return
         for p in dw.projections:
             x = dw.xs[p.x]
             plan = self.plans[p.name]
@@ -116,14 +134,20 @@ class Rotation:
     def check_status(self, stream):
         """Raise if a step launch of any plan gave up waiting (its y would be
         invalid, so its time must not count as throughput)."""
-        for h in self.plans.values():
+        for h in list(self.plans.values()) + list(self.multi.values()):
             self.L.lora_plan_status(h, stream)
 
     def release(self):
-        for h in self.plans.values():
+        for h in list(self.plans.values()) + list(self.multi.values()):
             self.L.lora_plan_destroy(h)
         for dw in self.copies:
             dw.release()
+
+
+def rot_groups(w):
+    """The launches of a step when the projections that share an input and
+    an output width run together."""
+    return sorted({(p.x, p.h_out) for p in w.projections})
 
 
 def footprint_bytes(w):
@@ -179,6 +203,9 @@ def measure(torch, w, dev, steps, warmup, rotate_mib, label):
     torch.cuda.synchronize()
     ms = time_graph(torch, rot, steps, warmup, "apply")
     log(f"[{label}] {steps} steps in {ms:.3f} ms")
+    ms_multi = time_graph(torch, rot, steps, warmup, "multi") if rot.multi else None
+    if ms_multi is not None:
+        log(f"[{label}] projections sharing an input in one launch: {ms_multi:.3f} ms")
     ms_shrink = time_graph(torch, rot, steps, warmup, "shrink")
     ms_expand = time_graph(torch, rot, steps, warmup, "expand")
     log(f"[{label}] shrink-only {ms_shrink:.3f} ms, expand-only {ms_expand:.3f} ms")
@@ -209,7 +236,7 @@ def measure(torch, w, dev, steps, warmup, rotate_mib, label):
         tokens_per_s=n_act * steps / (ms * 1e-3), n_active=n_act, distinct=int(used.size),
         shrink=dict(bytes=shrink_b, us=ms_shrink * 1e3 / (steps * n_proj)),
         expand=dict(bytes=expand_b, us=ms_expand * 1e3 / (steps * n_proj)),
-        n_proj=n_proj,
+        n_proj=n_proj, ms_multi=ms_multi,
     )
 
 
@@ -645,6 +672,14 @@ def main():
             "tokens_per_s": round(mx["tokens_per_s"], 1),
             "TFLOPs": round(mx["flops_per_step"] / (mx["ms_per_step"] * 1e-3) / 1e12, 3),
             "launches_per_step": mx["n_proj"],
+            **({} if mx["ms_multi"] is None else {
+                "shared_input_one_launch": {
+                    "ms_per_step": mx["ms_multi"] / mx["steps"],
+                    "GBps": round(mx["bytes_per_step"] / (mx["ms_multi"] / mx["steps"] * 1e-3) / 1e9, 2),
+                    "pct_hbm_peak": round(100.0 * mx["bytes_per_step"] / (mx["ms_multi"] / mx["steps"] * 1e-3)
+                                          / 1e9 / HBM_PEAK_GBPS, 2),
+                    "launches_per_step": len(rot_groups(wx)),
+                    "how": "lora_plan_apply_multi: the projections that share x (q/k/v, gate/up) in one grid"}}),
             "distinct_adapters": mx["distinct"],
             "algorithmic_bytes_per_step": mx["bytes_per_step"],
             "rotated_copies": mx["R"],

@@ -293,6 +293,30 @@ int lora_plan_expand(lora_plan_t p, lora_table_t t, void* y, int64_t ldy, void* 
 int lora_plan_destroy(lora_plan_t p);
 
 /*
+ * Projections that share their input (Section 4.1's adapter on several
+ * weights of a layer: q, k and v on the attention input; gate and up on the
+ * MLP input), run as one launch.  lora_plan_create_multi plans the batch on
+ * tables[0] once and lays the work out n times (n in [1, 4]), each copy with
+ * its own partial blocks and counters; every tables[i] must agree with
+ * tables[0] in h_in, h_out, dtype and the ranks of the adapters the batch
+ * references.  lora_plan_apply_multi then runs, in one grid,
+ *
+ *     ys[i][t, :] = round(ys[i][t, :] + s_g (x[t, :] . A_g^(i)) . B_g^(i))
+ *
+ * for every projection i < n (the plan's n) with the factors of tables[i]
+ * (tables[0] NULL: the plan's own), each copy's items waiting only on items of
+ * the same copy.  Results equal n lora_plan_apply launches bit for bit.  The
+ * ys must not overlap x or each other.  Recordable in a HIP graph, like
+ * lora_plan_apply; lora_plan_status reports its give-ups.  Such a plan is
+ * refused by lora_plan_apply, _shrink, _expand and lora_plan_update
+ * (LORA_E_ARG): create another for a new batch.
+ */
+int lora_plan_create_multi(lora_plan_t* out, int32_t n, const lora_table_t* tables, const lora_batch_t* b,
+                           void* stream);
+int lora_plan_apply_multi(lora_plan_t p, const lora_table_t* tables, const void* x, int64_t ldx, void* const* ys,
+                          const int64_t* ldys, void* stream);
+
+/*
  * Status of the plan's launches so far: waits for `stream`, then returns
  * LORA_OK; LORA_E_SYNC when a lora_plan_apply launch gave up waiting (its y is
  * invalid); or LORA_E_STALE when a recorded launch of an earlier batch ran

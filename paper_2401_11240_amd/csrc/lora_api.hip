@@ -106,6 +106,8 @@ struct HostPlan {
     int n_groups = 0;
     int r_max = 0;
     int n_rb = 0;                       // row blocks
+    int n_proj = 1;                     // projections sharing x that one launch runs (copies of the lists)
+    std::vector<int64_t> rb_bytes;      // bytes each row block streams
     std::vector<int32_t> perm, group_off, group_adapter, group_rank;
     std::vector<DevItem> shrink, expand, reduce, reduce_all, step;
     int n_rows = 0;
@@ -173,7 +175,7 @@ void group_rows(const lora_batch_t* b, int n_adapters, std::vector<int32_t>& per
     }
 }
 
-int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
+int plan_lists(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     int rc = validate_batch(b, t->n);
     if (rc) return rc;
     p.h_in = t->h_in;
@@ -191,7 +193,9 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     p.reduce_all.clear();
     p.n_rows = b->n_rows;
     p.step.clear();
-    std::vector<int64_t> rb_bytes;          // bytes each row block streams
+    std::vector<int64_t>& rb_bytes = p.rb_bytes;
+    rb_bytes.clear();
+    p.n_proj = 1;
     p.n_partials = 0;
     p.n_rb = 0;
 
@@ -303,6 +307,42 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
         }
     }
 
+    return LORA_OK;
+}
+
+// The lists of one projection repeated for n projections that share x: copy c
+// carries c in its kind, its own partial and v blocks and its own row block
+// counters (offsets of c times one copy's).  Each copy's items wait only on
+// items of the same copy.
+void replicate_lists(HostPlan& p, int n) {
+    const int64_t np = p.n_partials;
+    const int nrb = p.n_rb;
+    auto rep = [&](std::vector<DevItem>& v) {
+        const size_t m = v.size();
+        v.reserve(m * n);
+        for (int c = 1; c < n; ++c)
+            for (size_t i = 0; i < m; ++i) {
+                DevItem it = v[i];
+                it.kind |= c << kProjShift;
+                it.part += c * np;
+                it.rb += c * nrb;
+                v.push_back(it);
+            }
+    };
+    rep(p.shrink);
+    rep(p.reduce);
+    rep(p.expand);
+    rep(p.reduce_all);
+    const std::vector<int64_t> rb0(p.rb_bytes);
+    for (int c = 1; c < n; ++c) p.rb_bytes.insert(p.rb_bytes.end(), rb0.begin(), rb0.end());
+    p.n_partials = np * n;
+    p.n_rb = nrb * n;
+    p.n_proj = n;
+}
+
+// The grid layout and the device layout of the lists, and the upload image.
+int plan_layout(const lora_table_s* t, HostPlan& p) {
+    const std::vector<int64_t>& rb_bytes = p.rb_bytes;
     if ((uint64_t)p.n_partials * 4 > kMaxSpan)
         return fail(LORA_E_SHAPE, "batch too large: its partial results exceed 2 GiB");
 
@@ -394,6 +434,19 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     put(p.off_step, p.step.data(), p.step.size() * sizeof(DevItem));
     put(p.off_perm, p.perm.data(), p.perm.size() * sizeof(int32_t));
     return LORA_OK;
+}
+
+int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
+    if (int rc = plan_lists(t, b, p)) return rc;
+    return plan_layout(t, p);
+}
+
+// One plan for n projections that share x, planned on the first table (the
+// others must agree with it in shapes and in the ranks the batch references).
+int build_plan_multi(const lora_table_s* t, int n, const lora_batch_t* b, HostPlan& p) {
+    if (int rc = plan_lists(t, b, p)) return rc;
+    replicate_lists(p, n);
+    return plan_layout(t, p);
 }
 
 // A table may run a plan made with another table when shapes, dtype and the
@@ -614,6 +667,28 @@ int enqueue(const lora_table_s* t, const HostPlan& p, unsigned char* w, const vo
 // Enqueue the whole step of plan p as one launch (shrink and expand items in
 // one grid).  The row block counters at w + off_sync must be zero and the
 // step partial blocks armed.
+// The arguments of the step launch of plan p (one projection).
+int step_args(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x, int64_t ldx, void* y,
+              int64_t ldy, int spin_limit, KernelArgs& out) {
+    KernelArgs a = make_args(t, p, w, spin_limit);
+    a.partials = (float*)(w + p.off_step_partials);
+    if (!p.step.empty()) {                    // the grid laid out per XCD
+        a.items = (const DevItem*)(w + p.off_step);
+        a.n_items = (int32_t)p.step.size();
+    } else {
+        a.items = (const DevItem*)(w + p.off_shrink);
+        a.n_items = (int32_t)(p.shrink.size() + p.reduce.size() + p.expand.size());
+    }
+    a.x = x;
+    a.ldx = ldx;
+    a.x_bytes = (uint32_t)span_bytes(p.n_rows, ldx, t->h_in);
+    a.y = y;
+    a.ldy = ldy;
+    a.y_bytes = (uint32_t)span_bytes(p.n_rows, ldy, t->h_out);
+    out = a;
+    return LORA_OK;
+}
+
 int enqueue_step(const lora_table_s* t, const HostPlan& p, unsigned char* w, const void* x,
                  int64_t ldx, void* y, int64_t ldy, int spin_limit, hipStream_t s) {
     KernelArgs a = make_args(t, p, w, spin_limit);
@@ -1244,10 +1319,16 @@ int lora_plan_bytes(lora_table_t t, const lora_batch_t* b, size_t* bytes) {
     return LORA_OK;
 }
 
-int lora_plan_create_reserved(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, size_t min_bytes,
-                              void* stream) {
+}  // extern "C"
+
+namespace {
+
+// A plan of n projections sharing x (n = 1: an ordinary plan).
+int plan_create(lora_plan_t* out, int n, const lora_table_t* tables, const lora_batch_t* b, size_t min_bytes,
+                void* stream) {
     if (!out) return fail(LORA_E_ARG, "out is NULL");
     *out = nullptr;
+    const lora_table_s* t = tables[0];
     if (int rc = check_table(t)) return rc;
     hipStream_t s = (hipStream_t)stream;
     if (int rc = check_not_capturing(s, "lora_plan_create")) return rc;
@@ -1255,9 +1336,19 @@ int lora_plan_create_reserved(lora_plan_t* out, lora_table_t t, const lora_batch
     if (!pl) return fail(LORA_E_NOMEM, "plan allocation failed");
     pl->table = t;
     pl->device = t->device;
-    if (int rc = build_plan(t, b, pl->plan)) {
+    if (int rc = n > 1 ? build_plan_multi(t, n, b, pl->plan) : build_plan(t, b, pl->plan)) {
         delete pl;
         return rc;
+    }
+    for (int i = 1; i < n; ++i) {
+        if (int rc = check_compatible(pl->plan, tables[i])) {
+            delete pl;
+            return rc;
+        }
+        if (tables[i]->device != t->device) {
+            delete pl;
+            return fail(LORA_E_ARG, "the projections' tables are on different devices");
+        }
     }
     pl->n_rows = b->n_rows;
     pl->capacity = align_up(std::max(pl->plan.plan_total_bytes, min_bytes));
@@ -1281,8 +1372,63 @@ int lora_plan_create_reserved(lora_plan_t* out, lora_table_t t, const lora_batch
     return LORA_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int lora_plan_create_reserved(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, size_t min_bytes,
+                              void* stream) {
+    return plan_create(out, 1, &t, b, min_bytes, stream);
+}
+
 int lora_plan_create(lora_plan_t* out, lora_table_t t, const lora_batch_t* b, void* stream) {
     return lora_plan_create_reserved(out, t, b, 0, stream);
+}
+
+int lora_plan_create_multi(lora_plan_t* out, int32_t n, const lora_table_t* tables, const lora_batch_t* b,
+                           void* stream) {
+    if (!out) return fail(LORA_E_ARG, "out is NULL");
+    *out = nullptr;
+    if (n < 1 || n > kMaxProj) return fail(LORA_E_ARG, "n must be in [1, " + std::to_string(kMaxProj) + "]");
+    if (!tables) return fail(LORA_E_ARG, "tables is NULL");
+    for (int i = 0; i < n; ++i)
+        if (int rc = check_table(tables[i])) return rc;
+    return plan_create(out, n, tables, b, 0, stream);
+}
+
+int lora_plan_apply_multi(lora_plan_t pl, const lora_table_t* tables, const void* x, int64_t ldx, void* const* ys,
+                          const int64_t* ldys, void* stream) {
+    if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
+    const int n = pl->plan.n_proj;
+    if (!tables || !ys || !ldys || !x) return fail(LORA_E_ARG, "tables, ys, ldys or x is NULL");
+    for (int i = 0; i < n; ++i) {
+        const lora_table_s* tt = tables[i] ? tables[i] : (i == 0 ? pl->table : nullptr);
+        if (!tt) return fail(LORA_E_ARG, "table " + std::to_string(i) + " is NULL");
+        if (int rc = check_compatible(pl->plan, tt)) return rc;
+        if (tt->device != pl->device) return fail(LORA_E_ARG, "table is on another device than the plan");
+        if (!ys[i]) return fail(LORA_E_ARG, "y " + std::to_string(i) + " is NULL");
+        if (pl->plan.n_active == 0) continue;
+        if (int rc = check_x(tt, x, ldx, pl->n_rows)) return rc;
+        if (int rc = check_y(tt, ys[i], ldys[i], pl->n_rows)) return rc;
+        if (int rc = check_overlap(x, ldx, tt->h_in, ys[i], ldys[i], tt->h_out, pl->n_rows)) return rc;
+        for (int j = 0; j < i; ++j)
+            if (int rc = check_overlap(ys[j], ldys[j], tt->h_out, ys[i], ldys[i], tt->h_out, pl->n_rows)) return rc;
+    }
+    if (pl->plan.n_active == 0) return LORA_OK;
+    const lora_table_s* t0 = tables[0] ? tables[0] : pl->table;
+    DeviceGuard dg(pl->device);
+    KernelArgs a{};
+    if (int rc = step_args(t0, pl->plan, pl->dmem, x, ldx, ys[0], ldys[0], pl->spin_limit, a)) return rc;
+    a.n_proj = n;
+    for (int i = 0; i < n; ++i) {
+        const lora_table_s* tt = tables[i] ? tables[i] : pl->table;
+        a.ptable[i] = tt->dev;
+        a.py[i] = ys[i];
+        a.pldy[i] = ldys[i];
+        a.py_bytes[i] = (uint32_t)span_bytes(pl->n_rows, ldys[i], tt->h_out);
+    }
+    LORA_HIP_TRY(launch_step(a, (const uint32_t*)pl->dmem, t0->dtype, (hipStream_t)stream));
+    return LORA_OK;
 }
 
 int lora_plan_update(lora_plan_t pl, lora_table_t t, const lora_batch_t* b, void* stream) {
@@ -1293,6 +1439,8 @@ int lora_plan_update(lora_plan_t pl, lora_table_t t, const lora_batch_t* b, void
     hipStream_t s = (hipStream_t)stream;
     DeviceGuard dg(pl->device);
     if (int rc = check_not_capturing(s, "lora_plan_update")) return rc;
+    if (pl->plan.n_proj > 1)
+        return fail(LORA_E_ARG, "a plan of several projections is re-planned with lora_plan_create_multi");
     HostPlan np;
     if (int rc = build_plan(tt, b, np)) return rc;
     if (np.plan_total_bytes > pl->capacity)
@@ -1308,6 +1456,7 @@ int lora_plan_update(lora_plan_t pl, lora_table_t t, const lora_batch_t* b, void
 static int plan_run(lora_plan_t pl, lora_table_t t, const void* x, int64_t ldx, void* y, int64_t ldy,
                     void* stream) {
     if (!pl || !pl->dmem) return fail(LORA_E_ARG, "plan is NULL");
+    if (pl->plan.n_proj > 1) return fail(LORA_E_ARG, "a plan of several projections runs through lora_plan_apply_multi");
     const lora_table_s* tt = t ? t : pl->table;
     if (int rc = check_compatible(pl->plan, tt)) return rc;
     if (tt->device != pl->device) return fail(LORA_E_ARG, "table is on another device than the plan");

@@ -120,6 +120,9 @@ struct DevItem {
 };
 static_assert(sizeof(DevItem) == 128, "DevItem layout");
 
+constexpr int kMaxProj = 4;       // projections one launch may carry (q, k, v; gate, up)
+constexpr int kProjShift = 8;     // DevItem::kind holds the projection above this bit
+
 struct KernelArgs {
     const DevItem* items;
     const int32_t* perm;        // grouped row order
@@ -142,8 +145,15 @@ struct KernelArgs {
     uint32_t x_bytes;           // bytes from x to the end of its last row (< 2 GiB)
     uint32_t y_bytes;           // bytes from y to the end of its last row (< 2 GiB)
     uint32_t generation;        // the work list these arguments were made for (header word 0)
+    int32_t n_proj;             // projections sharing x in this launch (items carry their projection)
     const void* gfac[2 * kKargGroups];   // per group g: [2g] = A_g, [2g + 1] = B_g
     float gscale[kKargGroups];           // per group: s_g
+    // launches of several projections sharing x: per projection, its adapter
+    // registry and its y (factor pointers are then read from the registry)
+    const DevAdapter* ptable[kMaxProj];
+    void* py[kMaxProj];
+    int64_t pldy[kMaxProj];
+    uint32_t py_bytes[kMaxProj];
 };
 static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 

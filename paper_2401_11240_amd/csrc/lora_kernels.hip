@@ -76,6 +76,10 @@ struct Item {
     int rows[kInlineRows];
     const void* fac;     // the factor this item streams: A_g (shrink) or B_g (expand)
     float scale;         // s_g
+    int proj;            // the item's projection (launches of several projections)
+    void* y;             // its y (such launches only)
+    int64_t ldy;
+    uint32_t y_bytes;
 };
 
 // The item's two 64-byte halves are requested together (two scalar loads in
@@ -87,7 +91,8 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     const u32x16 w1 = ((const u32x16*)p)[1];
     Item it;
     it.part = (int64_t)(((uint64_t)w0[1] << 32) | w0[0]);
-    it.kind = (int)w0[2];
+    it.kind = (int)(w0[2] & ((1u << kProjShift) - 1));
+    it.proj = (int)(w0[2] >> kProjShift);
     it.group = (int)w0[3];
     it.adapter = (int)w0[4];
     it.rank = (int)w0[5];
@@ -105,6 +110,9 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     for (int q = 0; q < kInlineRows; ++q) it.rows[q] = (int)w1[q];
     it.fac = nullptr;
     it.scale = 0.f;
+    it.y = nullptr;
+    it.ldy = 0;
+    it.y_bytes = 0;
     return it;
 }
 
@@ -124,15 +132,31 @@ enum : int {
     kLookupAuto = 0,     // the argument table for groups below kKargGroups, else the registry
     kLookupArgs = 1,     // the argument table only (the launch has at most kKargGroups groups)
     kLookupReg = 2,      // the device registry only
+    kLookupMulti = 3,    // the registry of the item's projection (launches of several projections)
 };
 
 // The factor this item streams and the group's scale.  The step kernel fixes
 // the source at compile time: a pointer that could point into either the
 // kernel arguments or the registry makes the compiler copy the arguments to
 // private memory.
+constexpr int kArgsOffset = 16;   // every kernel: the item list and header pointers, then KernelArgs
+
 template <int kLookup>
 __device__ __forceinline__ void resolve(const KernelArgs& a, Item& it) {
     const bool shrink = it.kind == kItemShrink;
+    if constexpr (kLookup == kLookupMulti) {
+        // per-projection fields, read through the argument segment with the
+        // item's (uniform) projection index
+        const unsigned char* kp = (const unsigned char*)__builtin_amdgcn_kernarg_segment_ptr() + kArgsOffset;
+        const int q = it.proj;
+        const DevAdapter* d = *(const DevAdapter* const*)(kp + offsetof(KernelArgs, ptable) + 8 * q) + it.adapter;
+        it.fac = shrink ? d->A : d->B;
+        it.scale = d->scale;
+        it.y = *(void* const*)(kp + offsetof(KernelArgs, py) + 8 * q);
+        it.ldy = *(const int64_t*)(kp + offsetof(KernelArgs, pldy) + 8 * q);
+        it.y_bytes = *(const uint32_t*)(kp + offsetof(KernelArgs, py_bytes) + 4 * q);
+        return;
+    }
     if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups)) {
         it.fac = a.gfac[2 * it.group + (shrink ? 0 : 1)];
         it.scale = a.gscale[it.group];
@@ -156,7 +180,6 @@ static_assert(2 * kKargGroups == 4 * 64 && kKargGroups == 2 * 64, "lane table sh
 // KernelArgs follow its 8-byte item pointer), not through the by-value
 // parameter: a lane-dependent index into the parameter can make the compiler
 // copy the whole argument block to private memory.
-constexpr int kArgsOffset = 16;   // every kernel: the item list and header pointers, then KernelArgs
 static_assert(alignof(KernelArgs) == 8, "kernel arguments: KernelArgs at offset 16");
 __device__ __forceinline__ LaneTable load_lane_table() {
     const int l = threadIdx.x & 63;
@@ -582,9 +605,13 @@ __global__ void __launch_bounds__(kThreads) lora_reduce_kernel(const DevItem* __
 // 8g .. 8g+7 and 32 + 8g .. 32 + 8g + 7 of its row (g = lane / 16).
 __device__ __forceinline__ int col_base(int m) { return 8 * (m >> 2) + 32 * ((m >> 1) & 1) + 4 * (m & 1); }
 
-template <class Fmt, int Q, int KSG, int MS, bool kSync>
+template <class Fmt, int Q, int KSG, int MS, bool kSync, bool kMulti = false>
 __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                                             unsigned char* smem) {
+    // the item's y: the launch's, or its projection's in a launch of several
+    void* const ybase = kMulti ? it.y : a.y;
+    const int64_t ldy = kMulti ? it.ldy : a.ldy;
+    const uint32_t ybytes = kMulti ? it.y_bytes : a.y_bytes;
     const int t = threadIdx.x;
     const int w = t >> 6;
     const int l = t & 63;
@@ -599,7 +626,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     const int nrows = it.nrows;
     const int h_out = a.h_out;
     u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v
-    const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
+    const rsrc_t yr = make_rsrc(ybase, ybytes);
     const rsrc_t br = make_rsrc((const uint16_t*)it.fac + it.lo, (uint32_t)(R * h_out - it.lo) * 2);
     const int rowv = lane_rows(a, it);
 
@@ -623,7 +650,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             const int r = p / TC;
             const int c = p - r * TC;
             const int row = row_of(rowv, r < nrows ? r : 0);
-            soff[i] = r < nrows && 8 * c + 8 <= len ? (int)(((int64_t)row * a.ldy + it.lo + 8 * c) * 2) : kOut;
+            soff[i] = r < nrows && 8 * c + 8 <= len ? (int)(((int64_t)row * ldy + it.lo + 8 * c) * 2) : kOut;
             ys[i] = bload16(yr, soff[i]);
         }
     } else {
@@ -636,7 +663,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
                 for (int h = 0; h < 2; ++h) {
                     const int c = (w + 4 * q) * 64 + 32 * h + 8 * lg;
                     const bool ok = m * 16 + lr < nrows && c + 8 <= len;
-                    yoff[q][m][h] = ok ? (int)(((int64_t)row * a.ldy + it.lo + c) * 2) : kOut;
+                    yoff[q][m][h] = ok ? (int)(((int64_t)row * ldy + it.lo + c) * 2) : kOut;
                 }
         }
 #pragma unroll
@@ -899,32 +926,32 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     }
 }
 
-template <class Fmt, bool kSync>
+template <class Fmt, bool kSync, bool kMulti = false>
 __device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
     const int ms = msub_body(it.nrows);
     const int q = expand_q(it.rank, it.nrows);
     const int ksg = expand_ksg(it.rank, it.nrows);
     if (ms == 1) {
-        if (q == 4) expand_body<Fmt, 4, 1, 1, kSync>(a, it, smem);
+        if (q == 4) expand_body<Fmt, 4, 1, 1, kSync, kMulti>(a, it, smem);
         else if (q == 2) {
-            if (ksg == 1) expand_body<Fmt, 2, 1, 1, kSync>(a, it, smem);
-            else expand_body<Fmt, 2, 2, 1, kSync>(a, it, smem);
+            if (ksg == 1) expand_body<Fmt, 2, 1, 1, kSync, kMulti>(a, it, smem);
+            else expand_body<Fmt, 2, 2, 1, kSync, kMulti>(a, it, smem);
         } else {
-            if (ksg == 2) expand_body<Fmt, 1, 2, 1, kSync>(a, it, smem);
-            else expand_body<Fmt, 1, 4, 1, kSync>(a, it, smem);
+            if (ksg == 2) expand_body<Fmt, 1, 2, 1, kSync, kMulti>(a, it, smem);
+            else expand_body<Fmt, 1, 4, 1, kSync, kMulti>(a, it, smem);
         }
     } else if (ms == 2) {
         if (q == 2) {
-            if (ksg == 1) expand_body<Fmt, 2, 1, 2, kSync>(a, it, smem);
-            else expand_body<Fmt, 2, 2, 2, kSync>(a, it, smem);
+            if (ksg == 1) expand_body<Fmt, 2, 1, 2, kSync, kMulti>(a, it, smem);
+            else expand_body<Fmt, 2, 2, 2, kSync, kMulti>(a, it, smem);
         } else {
-            if (ksg == 2) expand_body<Fmt, 1, 2, 2, kSync>(a, it, smem);
-            else expand_body<Fmt, 1, 4, 2, kSync>(a, it, smem);
+            if (ksg == 2) expand_body<Fmt, 1, 2, 2, kSync, kMulti>(a, it, smem);
+            else expand_body<Fmt, 1, 4, 2, kSync, kMulti>(a, it, smem);
         }
     } else {
-        if (ksg == 1) expand_body<Fmt, 1, 1, 4, kSync>(a, it, smem);
-        else if (ksg == 2) expand_body<Fmt, 1, 2, 4, kSync>(a, it, smem);
-        else expand_body<Fmt, 1, 4, 4, kSync>(a, it, smem);
+        if (ksg == 1) expand_body<Fmt, 1, 1, 4, kSync, kMulti>(a, it, smem);
+        else if (ksg == 2) expand_body<Fmt, 1, 2, 4, kSync, kMulti>(a, it, smem);
+        else expand_body<Fmt, 1, 4, 4, kSync, kMulti>(a, it, smem);
     }
 }
 
@@ -958,10 +985,11 @@ lora_step_kernel(const DevItem* __restrict__ items, const uint32_t* __restrict__
     } else {
         it = load_item(items + blockIdx.x);
         if (stale(hdr, a)) return;
-        if (it.kind == kItemShrink || it.kind == kItemExpand) resolve<kLookupReg>(a, it);
+        if (it.kind == kItemShrink || it.kind == kItemExpand) resolve<kLookup>(a, it);
     }
+    constexpr bool kMulti = kLookup == kLookupMulti;
     if (it.kind == kItemShrink) shrink_item<Fmt, true>(a, it, smem);
-    else if (it.kind == kItemExpand) expand_item<Fmt, true>(a, it, smem);
+    else if (it.kind == kItemExpand) expand_item<Fmt, true, kMulti>(a, it, smem);
     else if (it.kind == kItemReduce) reduce_body<true>(a, it, smem);
 }
 
@@ -990,7 +1018,10 @@ hipError_t launch_step(const KernelArgs& a, const uint32_t* hdr, int dtype, hipS
     if (a.n_items <= 0) return hipSuccess;
     const dim3 g(a.n_items), b(kThreads);
     const bool args = a.n_groups <= kKargGroups;
-    if (dtype == 0) {
+    if (a.n_proj > 1) {
+        if (dtype == 0) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupMulti>), g, b, 0, s, a.items, hdr, a);
+        else hipLaunchKernelGGL((lora_step_kernel<FmtBF16, kLookupMulti>), g, b, 0, s, a.items, hdr, a);
+    } else if (dtype == 0) {
         if (args) hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupArgs>), g, b, 0, s, a.items, hdr, a);
         else hipLaunchKernelGGL((lora_step_kernel<FmtF16, kLookupReg>), g, b, 0, s, a.items, hdr, a);
     } else {

@@ -40,6 +40,7 @@ EXPORTS = (
     "lora_expand", "lora_apply_fused", "lora_plan_create", "lora_plan_apply", "lora_plan_destroy",
     "lora_plan_shrink", "lora_plan_expand", "lora_plan_status", "lora_plan_set_spin_limit",
     "lora_plan_bytes", "lora_plan_create_reserved", "lora_plan_update", "lora_apply_fused_static",
+    "lora_plan_create_multi", "lora_plan_apply_multi",
     "lora_base_workspace_bytes", "lora_base_apply", "lora_base_plan_create", "lora_base_plan_apply",
     "lora_base_plan_destroy",
     "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
@@ -114,6 +115,8 @@ def load():
         "lora_plan_create_reserved": [C.POINTER(vp), vp, C.POINTER(_Batch), sz, vp],
         "lora_plan_update": [vp, vp, C.POINTER(_Batch), vp],
         "lora_plan_apply": [vp, vp, vp, i64, vp, i64, vp],
+        "lora_plan_create_multi": [C.POINTER(vp), i32, C.POINTER(vp), C.POINTER(_Batch), vp],
+        "lora_plan_apply_multi": [vp, C.POINTER(vp), vp, i64, C.POINTER(vp), C.POINTER(i64), vp],
         "lora_plan_destroy": [vp],
         "lora_plan_shrink": [vp, vp, vp, i64, vp],
         "lora_plan_expand": [vp, vp, vp, i64, vp],
@@ -264,6 +267,24 @@ def lora_plan_update(plan: int, table, batch: Batch, stream=None) -> None:
 def lora_plan_apply(plan: int, table, x, ldx: int, y, ldy: int, stream=None) -> None:
     """``table`` None = the table the plan was made with."""
     _check(load().lora_plan_apply(plan, table or None, _addr(x), ldx, _addr(y), ldy, _stream(stream)))
+
+
+def lora_plan_create_multi(tables, batch: Batch, stream=None) -> int:
+    """One plan for projections that share x (their tables, in order)."""
+    n = len(tables)
+    T = (C.c_void_p * max(1, n))(*[int(t) for t in tables])
+    out = C.c_void_p()
+    _check(load().lora_plan_create_multi(C.byref(out), n, T, batch.c, _stream(stream)))
+    return int(out.value or 0)
+
+
+def lora_plan_apply_multi(plan: int, tables, x, ldx: int, ys, ldys, stream=None) -> None:
+    """Every projection of a plan from lora_plan_create_multi, in one launch."""
+    n = len(ys)
+    T = (C.c_void_p * max(1, n))(*[int(t or 0) for t in tables])
+    Y = (C.c_void_p * max(1, n))(*[_addr(y) for y in ys])
+    LD = (C.c_int64 * max(1, n))(*[int(v) for v in ldys])
+    _check(load().lora_plan_apply_multi(plan, T, _addr(x), ldx, Y, LD, _stream(stream)))
 
 
 def lora_plan_shrink(plan: int, table, x, ldx: int, stream=None) -> None:
