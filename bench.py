@@ -99,9 +99,7 @@ class Rotation:
         first = self.copies[0]
         self.plans = {p.name: L.lora_plan_create(p.table, first.batch, stream) for p in first.projections}
         # projections that share an input: one plan of all of them, one launch
-        self.groups = {}
-        for i, p in enumerate(first.projections):
-            self.groups.setdefault((p.x, p.h_out), []).append(i)
+        self.groups = shared_input_groups(w)
         self.multi = {k: L.lora_plan_create_multi([first.projections[i].table for i in ix], first.batch, stream)
                       for k, ix in self.groups.items() if len(ix) > 1}
 
@@ -144,10 +142,20 @@ class Rotation:
             dw.release()
 
 
-def rot_groups(w):
-    """The launches of a step when the projections that share an input and
-    an output width run together."""
-    return sorted({(p.x, p.h_out) for p in w.projections})
+MAX_PROJ_PER_LAUNCH = 4
+
+
+def shared_input_groups(w):
+    """The launches of a step when the projections that share an input run
+    together, at most MAX_PROJ_PER_LAUNCH in one launch: {(x, k): [index]}."""
+    by_x = {}
+    for i, p in enumerate(w.projections):
+        by_x.setdefault(p.x, []).append(i)
+    out = {}
+    for x, ix in by_x.items():
+        for k in range(0, len(ix), MAX_PROJ_PER_LAUNCH):
+            out[(x, k)] = ix[k:k + MAX_PROJ_PER_LAUNCH]
+    return out
 
 
 def footprint_bytes(w):
@@ -678,7 +686,7 @@ def main():
                     "GBps": round(mx["bytes_per_step"] / (mx["ms_multi"] / mx["steps"] * 1e-3) / 1e9, 2),
                     "pct_hbm_peak": round(100.0 * mx["bytes_per_step"] / (mx["ms_multi"] / mx["steps"] * 1e-3)
                                           / 1e9 / HBM_PEAK_GBPS, 2),
-                    "launches_per_step": len(rot_groups(wx)),
+                    "launches_per_step": len(shared_input_groups(wx)),
                     "how": "lora_plan_apply_multi: the projections that share x (q/k/v, gate/up) in one grid"}}),
             "distinct_adapters": mx["distinct"],
             "algorithmic_bytes_per_step": mx["bytes_per_step"],

@@ -107,6 +107,7 @@ struct HostPlan {
     int r_max = 0;
     int n_rb = 0;                       // row blocks
     int n_proj = 1;                     // projections sharing x that one launch runs (copies of the lists)
+    std::vector<int> proj_h_out;        // their h_out (n_proj > 1)
     std::vector<int64_t> rb_bytes;      // bytes each row block streams
     std::vector<int32_t> perm, group_off, group_adapter, group_rank;
     std::vector<DevItem> shrink, expand, reduce, reduce_all, step;
@@ -310,34 +311,28 @@ int plan_lists(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     return LORA_OK;
 }
 
-// The lists of one projection repeated for n projections that share x: copy c
+// The lists of n projections that share x, one after the other: projection c
 // carries c in its kind, its own partial and v blocks and its own row block
-// counters (offsets of c times one copy's).  Each copy's items wait only on
-// items of the same copy.
-void replicate_lists(HostPlan& p, int n) {
+// counters (offsets past the projections before it).  Each projection's
+// items wait only on items of the same projection.
+void append_lists(HostPlan& p, const HostPlan& q, int c) {
     const int64_t np = p.n_partials;
     const int nrb = p.n_rb;
-    auto rep = [&](std::vector<DevItem>& v) {
-        const size_t m = v.size();
-        v.reserve(m * n);
-        for (int c = 1; c < n; ++c)
-            for (size_t i = 0; i < m; ++i) {
-                DevItem it = v[i];
-                it.kind |= c << kProjShift;
-                it.part += c * np;
-                it.rb += c * nrb;
-                v.push_back(it);
-            }
+    auto app = [&](std::vector<DevItem>& dst, const std::vector<DevItem>& src) {
+        for (DevItem it : src) {
+            it.kind |= c << kProjShift;
+            it.part += np;
+            it.rb += nrb;
+            dst.push_back(it);
+        }
     };
-    rep(p.shrink);
-    rep(p.reduce);
-    rep(p.expand);
-    rep(p.reduce_all);
-    const std::vector<int64_t> rb0(p.rb_bytes);
-    for (int c = 1; c < n; ++c) p.rb_bytes.insert(p.rb_bytes.end(), rb0.begin(), rb0.end());
-    p.n_partials = np * n;
-    p.n_rb = nrb * n;
-    p.n_proj = n;
+    app(p.shrink, q.shrink);
+    app(p.reduce, q.reduce);
+    app(p.expand, q.expand);
+    app(p.reduce_all, q.reduce_all);
+    p.rb_bytes.insert(p.rb_bytes.end(), q.rb_bytes.begin(), q.rb_bytes.end());
+    p.n_partials += q.n_partials;
+    p.n_rb += q.n_rb;
 }
 
 // The grid layout and the device layout of the lists, and the upload image.
@@ -441,12 +436,40 @@ int build_plan(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
     return plan_layout(t, p);
 }
 
-// One plan for n projections that share x, planned on the first table (the
-// others must agree with it in shapes and in the ranks the batch references).
-int build_plan_multi(const lora_table_s* t, int n, const lora_batch_t* b, HostPlan& p) {
-    if (int rc = plan_lists(t, b, p)) return rc;
-    replicate_lists(p, n);
-    return plan_layout(t, p);
+// One plan for n projections that share x (the same h_in and dtype, the
+// batch's adapters of the same ranks in every table; h_out may differ).
+int build_plan_multi(const lora_table_s* const* t, int n, const lora_batch_t* b, HostPlan& p) {
+    if (int rc = plan_lists(t[0], b, p)) return rc;
+    p.proj_h_out.assign(1, t[0]->h_out);
+    for (int c = 1; c < n; ++c) {
+        if (t[c]->h_in != t[0]->h_in || t[c]->dtype != t[0]->dtype)
+            return fail(LORA_E_SHAPE, "the projections differ in h_in or dtype");
+        HostPlan q;
+        if (int rc = plan_lists(t[c], b, q)) return rc;
+        append_lists(p, q, c);
+        p.proj_h_out.push_back(t[c]->h_out);
+    }
+    p.n_proj = n;
+    return plan_layout(t[0], p);
+}
+
+int check_compatible(const HostPlan& p, const lora_table_s* t);
+
+// Projection i of a plan of several projections: its table must agree with
+// the plan in h_in, dtype, its projection's h_out and the referenced ranks.
+int check_compatible_proj(const HostPlan& p, const lora_table_s* t, int i) {
+    if (!t || !t->dev) return fail(LORA_E_ARG, "table is NULL or released");
+    if (p.n_proj > 1 && t->h_out != p.proj_h_out[i])
+        return fail(LORA_E_SHAPE, "table " + std::to_string(i) + " has another h_out than its projection in the plan");
+    if (p.n_proj <= 1) return check_compatible(p, t);
+    if (t->h_in != p.h_in || t->dtype != p.dtype) return fail(LORA_E_SHAPE, "table shape or dtype differs from the plan's");
+    for (int g = 0; g < p.n_groups; ++g) {
+        const int a = p.group_adapter[g];
+        if (a >= t->n) return fail(LORA_E_INDEX, "table has fewer adapters than the plan references");
+        if (t->host[a].rank != p.group_rank[g])
+            return fail(LORA_E_RANK, "adapter " + std::to_string(a) + " has another rank than in the plan");
+    }
+    return LORA_OK;
 }
 
 // A table may run a plan made with another table when shapes, dtype and the
@@ -1336,20 +1359,20 @@ int plan_create(lora_plan_t* out, int n, const lora_table_t* tables, const lora_
     if (!pl) return fail(LORA_E_NOMEM, "plan allocation failed");
     pl->table = t;
     pl->device = t->device;
-    if (int rc = n > 1 ? build_plan_multi(t, n, b, pl->plan) : build_plan(t, b, pl->plan)) {
-        delete pl;
-        return rc;
-    }
-    for (int i = 1; i < n; ++i) {
-        if (int rc = check_compatible(pl->plan, tables[i])) {
-            delete pl;
-            return rc;
-        }
+    for (int i = 1; i < n; ++i)
         if (tables[i]->device != t->device) {
             delete pl;
             return fail(LORA_E_ARG, "the projections' tables are on different devices");
         }
+    if (int rc = n > 1 ? build_plan_multi(tables, n, b, pl->plan) : build_plan(t, b, pl->plan)) {
+        delete pl;
+        return rc;
     }
+    for (int i = 1; i < n; ++i)
+        if (int rc = check_compatible_proj(pl->plan, tables[i], i)) {
+            delete pl;
+            return rc;
+        }
     pl->n_rows = b->n_rows;
     pl->capacity = align_up(std::max(pl->plan.plan_total_bytes, min_bytes));
     DeviceGuard dg(t->device);
@@ -1404,7 +1427,7 @@ int lora_plan_apply_multi(lora_plan_t pl, const lora_table_t* tables, const void
     for (int i = 0; i < n; ++i) {
         const lora_table_s* tt = tables[i] ? tables[i] : (i == 0 ? pl->table : nullptr);
         if (!tt) return fail(LORA_E_ARG, "table " + std::to_string(i) + " is NULL");
-        if (int rc = check_compatible(pl->plan, tt)) return rc;
+        if (int rc = check_compatible_proj(pl->plan, tt, i)) return rc;
         if (tt->device != pl->device) return fail(LORA_E_ARG, "table is on another device than the plan");
         if (!ys[i]) return fail(LORA_E_ARG, "y " + std::to_string(i) + " is NULL");
         if (pl->plan.n_active == 0) continue;
@@ -1412,7 +1435,9 @@ int lora_plan_apply_multi(lora_plan_t pl, const lora_table_t* tables, const void
         if (int rc = check_y(tt, ys[i], ldys[i], pl->n_rows)) return rc;
         if (int rc = check_overlap(x, ldx, tt->h_in, ys[i], ldys[i], tt->h_out, pl->n_rows)) return rc;
         for (int j = 0; j < i; ++j)
-            if (int rc = check_overlap(ys[j], ldys[j], tt->h_out, ys[i], ldys[i], tt->h_out, pl->n_rows)) return rc;
+            if (int rc = check_overlap(ys[j], ldys[j], pl->plan.proj_h_out.empty() ? tt->h_out : pl->plan.proj_h_out[j],
+                                       ys[i], ldys[i], tt->h_out, pl->n_rows))
+                return rc;
     }
     if (pl->plan.n_active == 0) return LORA_OK;
     const lora_table_s* t0 = tables[0] ? tables[0] : pl->table;
@@ -1426,6 +1451,7 @@ int lora_plan_apply_multi(lora_plan_t pl, const lora_table_t* tables, const void
         a.py[i] = ys[i];
         a.pldy[i] = ldys[i];
         a.py_bytes[i] = (uint32_t)span_bytes(pl->n_rows, ldys[i], tt->h_out);
+        a.ph_out[i] = tt->h_out;
     }
     LORA_HIP_TRY(launch_step(a, (const uint32_t*)pl->dmem, t0->dtype, (hipStream_t)stream));
     return LORA_OK;

@@ -154,6 +154,7 @@ struct KernelArgs {
     void* py[kMaxProj];
     int64_t pldy[kMaxProj];
     uint32_t py_bytes[kMaxProj];
+    int32_t ph_out[kMaxProj];
 };
 static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 

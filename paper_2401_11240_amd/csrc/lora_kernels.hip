@@ -77,9 +77,10 @@ struct Item {
     const void* fac;     // the factor this item streams: A_g (shrink) or B_g (expand)
     float scale;         // s_g
     int proj;            // the item's projection (launches of several projections)
-    void* y;             // its y (such launches only)
+    void* y;             // its y and h_out (such launches only)
     int64_t ldy;
     uint32_t y_bytes;
+    int h_out;
 };
 
 // The item's two 64-byte halves are requested together (two scalar loads in
@@ -113,6 +114,7 @@ __device__ __forceinline__ Item load_item(const DevItem* __restrict__ p) {
     it.y = nullptr;
     it.ldy = 0;
     it.y_bytes = 0;
+    it.h_out = 0;
     return it;
 }
 
@@ -155,6 +157,7 @@ __device__ __forceinline__ void resolve(const KernelArgs& a, Item& it) {
         it.y = *(void* const*)(kp + offsetof(KernelArgs, py) + 8 * q);
         it.ldy = *(const int64_t*)(kp + offsetof(KernelArgs, pldy) + 8 * q);
         it.y_bytes = *(const uint32_t*)(kp + offsetof(KernelArgs, py_bytes) + 4 * q);
+        it.h_out = *(const int32_t*)(kp + offsetof(KernelArgs, ph_out) + 4 * q);
         return;
     }
     if (kLookup == kLookupArgs || (kLookup == kLookupAuto && it.group < kKargGroups)) {
@@ -624,7 +627,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     const int KS = round_up_i(R, 16) / 16;
     const int len = it.len;
     const int nrows = it.nrows;
-    const int h_out = a.h_out;
+    const int h_out = kMulti ? it.h_out : a.h_out;
     u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v
     const rsrc_t yr = make_rsrc(ybase, ybytes);
     const rsrc_t br = make_rsrc((const uint16_t*)it.fac + it.lo, (uint32_t)(R * h_out - it.lo) * 2);

@@ -2,8 +2,10 @@
 lora_plan_apply_multi): every projection's y equals its own lora_plan_apply
 launch bit for bit (whose results the full-size parity tests compare with the
 oracle on every row), on the 13B-shaped layer (q, k, v on one input; gate
-and up on another), on a decode-sized batch (the grid laid out per XCD) and a
-prompt-sized one (several projections of ragged width), eagerly and from a
+and up on another), on the 70B-shaped batch (q and gate, outputs of
+different widths, on one input), on a decode-sized batch (the grid laid out
+per XCD) and prompt-sized ones (projections of ragged and of different
+widths), eagerly and from a
 recorded graph replayed with eager work between replays; the rows are also
 compared with the oracle on the small cases; malformed calls are refused
 before anything runs."""
@@ -38,7 +40,7 @@ def say(*a):
 def groups(w):
     g = {}
     for i, p in enumerate(w.projections):
-        g.setdefault((p.x, p.h_out), []).append(i)
+        g.setdefault((p.x,), []).append(i)
     return {k: v for k, v in g.items() if len(v) > 1}
 
 
@@ -115,15 +117,22 @@ def test_13b_layer_shared_inputs_in_one_launch():
     check_workload(W.NAMED["llama13b_layer"]())
 
 
-@pytest.mark.parametrize("kind", ["decode", "prompt"])
+def test_70b_batch_q_and_gate_in_one_launch():
+    check_workload(W.NAMED["llama70b_mixed"](), graph_replays=1)
+
+
+@pytest.mark.parametrize("kind", ["decode", "prompt", "widths"])
 def test_small_batches_shared_input(kind):
     if kind == "decode":
         lens, sa = [1] * 40, [i % 7 for i in range(40)]
     else:
         lens, sa = [100, 37, 300, 5], [0, 3, 5, -1]
-    w = W.build_workload(name=f"multi_{kind}", seed=31, dtype=W.BF16 if kind == "prompt" else W.F16, n_adapters=7,
-                         rank_set=[8, 16, 40, 64], seg_adapter=sa, seg_lens=lens,
-                         projections=(("q", 520, 264, "x"), ("k", 520, 264, "x"), ("v", 520, 264, "x")))
+    if kind == "widths":   # output widths that differ: q, gate, up and a narrow k
+        projs = (("q", 520, 264, "x"), ("gate", 520, 776, "x"), ("up", 520, 776, "x"), ("k", 520, 72, "x"))
+    else:
+        projs = (("q", 520, 264, "x"), ("k", 520, 264, "x"), ("v", 520, 264, "x"))
+    w = W.build_workload(name=f"multi_{kind}", seed=31, dtype=W.F16 if kind == "decode" else W.BF16, n_adapters=7,
+                         rank_set=[8, 16, 40, 64], seg_adapter=sa, seg_lens=lens, projections=projs)
     check_workload(w, against_oracle=True)
 
 
@@ -136,12 +145,16 @@ def test_multi_refuses_bad_calls():
     x = dw.xs["x"]
     s = torch.cuda.current_stream(DEV)
     try:
-        with pytest.raises(L.LoraError) as e:      # another output width
-            L.lora_plan_create_multi([q.table, o.table], dw.batch, s)
-        assert e.value.code == L.LORA_E_SHAPE
         with pytest.raises(L.LoraError) as e:
             L.lora_plan_create_multi([], dw.batch, s)
         assert e.value.code == L.LORA_E_ARG
+        h = L.lora_plan_create_multi([q.table, o.table], dw.batch, s)
+        try:
+            with pytest.raises(L.LoraError) as e:  # a table of another output width in a projection's place
+                L.lora_plan_apply_multi(h, [q.table, k.table], x, 256, [q.y, k.y], [128, 128], s)
+            assert e.value.code == L.LORA_E_SHAPE
+        finally:
+            L.lora_plan_destroy(h)
         h = L.lora_plan_create_multi([q.table, k.table], dw.batch, s)
         try:
             with pytest.raises(L.LoraError) as e:  # outputs overlapping each other
