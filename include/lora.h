@@ -295,18 +295,22 @@ int lora_plan_destroy(lora_plan_t p);
 /*
  * Projections that share their input (Section 4.1's adapter on several
  * weights of a layer: q, k and v on the attention input; gate and up on the
- * MLP input), run as one launch.  lora_plan_create_multi plans the batch on
- * tables[0] once and lays the work out n times (n in [1, 4]), each copy with
- * its own partial blocks and counters; every tables[i] must agree with
- * tables[0] in h_in, h_out, dtype and the ranks of the adapters the batch
- * references.  lora_plan_apply_multi then runs, in one grid,
+ * MLP input; q and gate when both read one input), run as one launch.
+ * lora_plan_create_multi plans the batch on each tables[i] (n in [1, 4]) and
+ * lays the n work lists out one after the other, each with its own partial
+ * blocks and counters; every tables[i] must agree with tables[0] in h_in,
+ * dtype and the ranks of the adapters the batch references (LORA_E_SHAPE,
+ * LORA_E_RANK otherwise); h_out may differ.  lora_plan_apply_multi then runs,
+ * in one grid,
  *
  *     ys[i][t, :] = round(ys[i][t, :] + s_g (x[t, :] . A_g^(i)) . B_g^(i))
  *
  * for every projection i < n (the plan's n) with the factors of tables[i]
- * (tables[0] NULL: the plan's own), each copy's items waiting only on items of
- * the same copy.  Results equal n lora_plan_apply launches bit for bit.  The
- * ys must not overlap x or each other.  Recordable in a HIP graph, like
+ * (tables[0] NULL: the plan's own), which must have the h_out of projection i
+ * at plan creation (LORA_E_SHAPE), each projection's items waiting only on
+ * items of the same projection; ys[i] is [n_rows, ldys[i]] with ldys[i] >=
+ * that h_out.  Results equal n lora_plan_apply launches bit for bit.  The ys
+ * must not overlap x or each other.  Recordable in a HIP graph, like
  * lora_plan_apply; lora_plan_status reports its give-ups.  Such a plan is
  * refused by lora_plan_apply, _shrink, _expand and lora_plan_update
  * (LORA_E_ARG): create another for a new batch.
