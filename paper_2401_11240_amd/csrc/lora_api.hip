@@ -263,8 +263,8 @@ int plan_lists(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
                 it.part = part0 + (int64_t)c * pstride;
                 it.lo = c * krange;
                 it.len = std::min(krange, t->h_in - c * krange);
-                it.sub = sub;
-                if (shrink_lds_bytes(r, sub, nb) > kShrinkLds)
+                it.sub = shrink_uses_dma(r, nb) ? shrink_stage_sub(r, nb) : sub;
+                if (!shrink_uses_dma(r, nb) && shrink_lds_bytes(r, sub, nb) > kShrinkLds)
                     return fail(LORA_E_SHAPE, "internal: shrink tile exceeds LDS");
                 p.shrink.push_back(it);
             }
@@ -301,7 +301,7 @@ int plan_lists(const lora_table_s* t, const lora_batch_t* b, HostPlan& p) {
                 it.sub = direct ? 1 : 0;
                 it.lo = c * nlen;
                 it.len = std::min(nlen, t->h_out - c * nlen);
-                if (expand_lds_bytes(r, nb) > kExpandVmaxOff)
+                if (!expand_fits_lds(r, nb))
                     return fail(LORA_E_SHAPE, "internal: expand tile exceeds LDS");
                 p.expand.push_back(it);
             }

@@ -54,11 +54,15 @@ constexpr int kThreads = 256;            // workgroup size: 4 wave64
 constexpr int kMaxRank = 256;
 constexpr int kInlineRows = 16;          // items this small carry their rows inline
 constexpr int kKargGroups = 128;         // groups whose pointers travel in the kernel arguments
-constexpr int kShrinkLds = 52 * 1024;    // LDS bytes of the shrink body
-constexpr int kExpandLds = 34 * 1024;    // LDS bytes of the expand body (v fragments, then the y tile)
-constexpr int kExpandVmaxOff = kExpandLds - 16;   // expand: per-wave largest |v| (4 floats) after the fragments
+constexpr int kShrinkStages = 4;         // LDS buffers of the direct-to-LDS shrink
+constexpr int kStageChunks = 1024;       // 16-byte chunks per buffer (one 16 KiB pass)
+constexpr int kShrinkLds = kShrinkStages * kStageChunks * 16;   // LDS bytes of the shrink bodies
+constexpr int kExpandYsOff = 32 * 1024;  // expand: v fragments below, the staged y tile from here
+constexpr int kExpandLds = kExpandYsOff + 33 * 1024 + 256;   // LDS bytes of the expand body
+constexpr int kExpandVmaxOff = kExpandLds - 16;   // expand: per-wave largest |v| (4 floats) after the y tile
+constexpr int kExpandTiles = 2;          // column tiles of a prompt expand item
 constexpr int kReduceLds = kThreads * 16;
-constexpr int kStepLds = kShrinkLds;
+constexpr int kStepLds = kShrinkLds > kExpandLds ? kShrinkLds : kExpandLds;
 constexpr int kSyncStride = 32;          // 32-bit words between row block counters (one 128-byte line each)
 constexpr int kReduceBytes = 32 * 1024;  // partial bytes one reduce item adds up at most
 constexpr int kDirectBytes = 16 * 1024;  // partial bytes up to which expand items add them up themselves
@@ -258,6 +262,24 @@ LORA_HD inline int shrink_sub(int rank, int nrows) {
     return max_i(32, k);
 }
 
+// K per pass of the direct-to-LDS shrink (ranks that are a multiple of 8):
+// the largest multiple of 64 (else 32) up to 512 whose A rows (rounded to
+// whole 1 KiB wave loads) and x rows fit one buffer; 0 when none does (the
+// register-staged body then runs the item).
+LORA_HD inline int shrink_stage_sub(int rank, int nrows) {
+    if (rank % 8 != 0) return 0;
+    const int ms = msub_body(nrows);
+    for (int k = 512; k >= 32; k -= (k > 64 ? 64 : 32))
+        if (round_up_i(k * (rank / 8), 64) + 2 * ms * k <= kStageChunks) return k;
+    return 0;
+}
+// Only row blocks of more than one 16-row subtile stream through the LDS
+// buffers; a decode block's pass is one memory round trip either way, and the
+// register-staged body measured faster there.
+LORA_HD inline bool shrink_uses_dma(int rank, int nrows) {
+    return msub_body(nrows) > 1 && shrink_stage_sub(rank, nrows) >= 32;
+}
+
 // ---- expand ----
 // Column tiles of 256 * q columns (q column blocks of 64 per wave) with
 // q * msub <= 4 (registers) and a B tile of about 32 KiB.  Ranks are taken in
@@ -273,18 +295,25 @@ LORA_HD inline int expand_q(int rank, int nrows) {
 }
 LORA_HD inline int expand_ksg(int rank, int nrows) {
     const int ks = round_up_i(rank, 16) / 16;
-    const int cap = 4 / expand_q(rank, nrows);
+    // items of four subtiles keep the next group's B in flight beside their
+    // accumulators: groups of at most 2 steps
+    const int cap = msub_body(nrows) >= 4 ? 2 : 4 / expand_q(rank, nrows);
     return ks >= cap ? cap : (ks >= 2 ? 2 : 1);
 }
-LORA_HD inline int expand_nlen(int rank, int nrows) { return 256 * expand_q(rank, nrows); }
-// v fragments; for items of more than one 16-row subtile also the y tile
-// staged through LDS afterwards ([rows][256 q / 8 + 1] chunks of 16 bytes, in
-// the same space).
-LORA_HD inline int expand_lds_bytes(int rank, int nrows) {
+// Columns of an expand item: one tile of 256 q, or kExpandTiles tiles for
+// items of four 16-row subtiles (they make their v fragments once).
+LORA_HD inline int expand_tile(int rank, int nrows) { return 256 * expand_q(rank, nrows); }
+LORA_HD inline int expand_nlen(int rank, int nrows) {
+    return expand_tile(rank, nrows) * (msub_body(nrows) == 4 ? kExpandTiles : 1);
+}
+// The v fragments (below kExpandYsOff) and, for items of more than one
+// 16-row subtile, the y tile staged through LDS ([rows][256 q / 8 + 1] chunks
+// of 16 bytes, from kExpandYsOff) fit the expand's LDS.
+LORA_HD inline bool expand_fits_lds(int rank, int nrows) {
     const int ms = msub_body(nrows);
     const int vf = ms * (round_up_i(rank, 16) / 16) * 64 * 16;
     const int yt = ms > 1 ? ms * 16 * (32 * expand_q(rank, nrows) + 1) * 16 : 0;
-    return max_i(vf, yt);
+    return vf <= kExpandYsOff && kExpandYsOff + yt <= kExpandVmaxOff;
 }
 
 }  // namespace lora

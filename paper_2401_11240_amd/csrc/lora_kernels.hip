@@ -499,10 +499,297 @@ __device__ __forceinline__ void shrink_body(const KernelArgs& a, const Item& it,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Shrink with direct-to-LDS staging (ranks that are a multiple of 8).  Each
+// pass brings `sub` K of the item's A rows and x rows into one of
+// kShrinkStages LDS buffers by buffer-to-LDS loads (no registers, no VALU
+// work), up to kShrinkStages passes ahead of the MFMAs.  A stays as stored,
+// [K][rank] with ranks contiguous: its MFMA operand (8 consecutive K of one
+// rank per lane) comes out of LDS through the transposing 64-bit read, two
+// per fragment.  x rows keep their K order: one 16-byte read is a fragment.
+//
+// Buffer layout, in 16-byte chunks: A chunk (k, c) (ranks 8c .. 8c + 7 of K
+// row k) at slot k cpr + (c ^ swa(k)), then, from the next multiple of 64,
+// x chunk (r, c) (K 8c .. 8c + 7 of the item's row r) at slot r cpx +
+// (c ^ (r & xmask)).  The swizzles spread a fragment read over the banks: the
+// 16 lanes of a transposing read cover 4 K rows x 32 bytes, those of an x
+// read 16 rows x 16 bytes.  Every slot a fragment read touches is rewritten
+// by each pass (chunks past the pass's K, the item's rows or the region read
+// as zeros), so nothing stale is ever used.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+
+// 16 bytes from buffer r at byte offset off (zeros when out of range) into
+// LDS at lds + 16 * lane; lds is the same for every lane of the wave.
+__device__ __forceinline__ void dma16(rsrc_t r, unsigned char* lds, int off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_u8*)lds, 16, off, 0, 0, 0);
+}
+// Transposing read: within each 16 lanes, lane j returns element j % 4 of the
+// 8-byte values that lanes j / 4, 4 + j / 4, 8 + j / 4, 12 + j / 4 address.
+// Written as inline assembly: for the builtin the compiler waits for every
+// buffer-to-LDS load in flight (later passes' too) before the read.  The
+// compiler does not count this read, so its value is used only after
+// lgkm_wait() on it; the compiler's own LDS waits stay correct, as LDS
+// operations complete in order and an uncounted one only makes them wait
+// longer.
+__device__ __forceinline__ u32x2 lds_read_tr16(const unsigned char* p) {
+    u32x2 v;
+    const uint32_t addr = (uint32_t)(uintptr_t)(lds_u8*)p;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+}
+// Every LDS read issued so far has completed, those of v among them.
+template <int N>
+__device__ __forceinline__ void lgkm_wait(u32x4 (&v)[N]) {
+    static_assert(N == 1 || N == 2 || N == 4, "fragments");
+    if constexpr (N == 1) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]));
+    else if constexpr (N == 2) asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]));
+    else asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
+}
+// s_waitcnt vmcnt(N), the other counters left free (gfx9 encoding: vmcnt
+// bits 3:0 and 15:14).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// LDS written by every wave (its own loads waited for) and read by none of
+// the earlier pass's fragment reads any more; later LDS reads stay after it.
+__device__ __forceinline__ void stage_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <class Fmt, int TQ, int MS, bool kSync>
+__device__ __forceinline__ void shrink_dma_body(const KernelArgs& a, const Item& it, unsigned char* smem) {
+    constexpr int S = kShrinkStages;
+    constexpr int kStageBytes = kStageChunks * 16;
+    constexpr int NL = kStageChunks / kThreads;   // loads per thread (and per wave) of one pass
+    static_assert(NL * kThreads == kStageChunks && NL * (S - 1) < 64, "stage loads");
+    const int t = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int lr = t & 15;
+    const int lg = (t >> 4) & 3;
+    uint32_t parity = 0;                      // step launch: which partial buffer (read first, used last)
+    if constexpr (kSync) parity = row_block_parity(a, it);
+    const int R = it.rank;                    // a multiple of 8: the partial row stride is R
+    const int Rp = round_up_i(R, 16);
+    const int NT = Rp / 16;
+    const int sub = it.sub;                   // K per pass, a multiple of 32
+    const int cpr = R / 8;
+    const int cpx = sub / 8;
+    const int nA = sub * cpr;
+    const int nAr = round_up_i(nA, 64);
+    const int nX = MS * 16 * cpx;
+    const int nrows = it.nrows;
+    const int WN = shrink_wn(R, nrows);
+    const int WK = 4 / WN;
+    const int wn = w % WN;
+    const int wk = w / WN;
+    // A swizzle swa(k) = ((k >> ash) << 1) & amask: 2 (k % 4) for 8 or more
+    // chunks per row, 2 ((k / 2) % 2) for 4, none otherwise (and for a chunk
+    // count that is not a power of two)
+    const int ash = cpr >= 8 ? 0 : 1;
+    const int amask = (cpr & (cpr - 1)) != 0 ? 0 : (cpr >= 8 ? 6 : (cpr == 4 ? 2 : 0));
+    const int xmask = (cpx & 7) == 0 ? 7 : 3;
+    // the loads take their resource from scalar registers: say that these
+    // values are the same in every lane
+    const uint64_t fa = (uint64_t)((const uint16_t*)it.fac + (int64_t)it.lo * R);
+    const void* fau = (const void*)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(fa >> 32)) << 32) |
+                                    (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)fa));
+    const rsrc_t ar = make_rsrc(fau, (uint32_t)__builtin_amdgcn_readfirstlane(it.len * R * 2));
+    const rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+    const int rowv = lane_rows(a, it);
+
+    // This thread's NL loads of a pass: chunk q = 256 i + t of the buffer;
+    // wave w's load i fills chunks 256 i + 64 w .. + 63 (one resource each).
+    int lbase[NL], lk[NL];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+        const int q = 256 * i + t;
+        const int qx = q - nAr;
+        const int r = qx >= 0 && qx < nX ? qx / cpx : 0;
+        const int row = row_of(rowv, r < nrows ? r : 0);   // every lane active
+        lbase[i] = kOut;
+        lk[i] = 0;
+        if (q < nA) {
+            const int k = q / cpr;
+            const int c = (q - k * cpr) ^ (((k >> ash) << 1) & amask);
+            lbase[i] = (k * R + 8 * c) * 2;
+            lk[i] = k;
+        } else if (qx >= 0 && qx < nX && r < nrows) {
+            const int c = (qx - r * cpx) ^ (r & xmask);
+            lbase[i] = (int)(((int64_t)row * a.ldx + it.lo + 8 * c) * 2);
+            lk[i] = 8 * c;
+        }
+    }
+    auto issue = [&](int pass) __attribute__((always_inline)) {
+        const int k0 = pass * sub;
+        const int plen = min_i(sub, it.len - k0);
+        unsigned char* st = smem + (pass % S) * kStageBytes;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+            const int cb = 256 * i + 64 * w;  // wave-uniform
+            const bool isA = cb < nAr;
+            const int off = lbase[i] != kOut && lk[i] < plen ? lbase[i] + (isA ? k0 * R * 2 : k0 * 2) : kOut;
+            dma16(isA ? ar : xr, st + cb * 16, off);
+        }
+    };
+
+    f32x4 acc[MS][TQ];
+#pragma unroll
+    for (int m = 0; m < MS; ++m)
+#pragma unroll
+        for (int q = 0; q < TQ; ++q) acc[m][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const u32x4 z4 = {0u, 0u, 0u, 0u};
+    const int npass = (it.len + sub - 1) / sub;
+    const int ksf = sub / 32;                 // K steps of a whole pass
+
+    const int pre = min_i(npass, S);
+    for (int p = 0; p < pre; ++p) issue(p);
+    for (int pass = 0; pass < npass; ++pass) {
+        // passes whose loads this wave issued after this one's
+        const int after = min_i(npass - 1, pass == 0 ? S - 1 : pass + S - 2) - pass;
+        if (after >= 3) wait_vm<(S > 3 ? 3 * NL : 0)>();
+        else if (after == 2) wait_vm<(S > 2 ? 2 * NL : 0)>();
+        else if (after == 1) wait_vm<NL>();
+        else wait_vm<0>();
+        stage_barrier();
+        if (pass >= 1 && pass + S - 1 < npass) issue(pass + S - 1);   // into the buffer pass - 1 used
+        const unsigned char* st = smem + (pass % S) * kStageBytes;
+        const int plen = min_i(sub, it.len - pass * sub);
+        const int ks = (plen + 31) / 32;
+        // the fragment reads of K step s; af is usable after lgkm_wait(af)
+        // and mask_a(af)
+        auto frags = [&](int s, u32x4 (&af)[TQ], u32x4 (&xf)[MS]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                const int col = tile * 16 + 4 * (lr & 3);     // the ranks this lane's reads address
+                const int cc = tile < NT && col < R ? col >> 3 : 0;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int k = 32 * s + 8 * lg + 4 * h + (lr >> 2);
+                    const int slot = k * cpr + (cc ^ (((k >> ash) << 1) & amask));
+                    const u32x2 v = lds_read_tr16(st + slot * 16 + (lr & 1) * 8);
+                    af[q][2 * h] = v.x;
+                    af[q][2 * h + 1] = v.y;
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < MS; ++m) {
+                const int row = m * 16 + lr;
+                const int c = (4 * s + lg) ^ (row & xmask);
+                xf[m] = *(const u32x4*)(st + (nAr + row * cpx + c) * 16);
+            }
+        };
+        auto mask_a = [&](u32x4 (&af)[TQ]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                // this lane's operand is rank tile * 16 + lr
+                if (!(tile < NT && tile * 16 + lr < R)) af[q] = z4;
+            }
+        };
+        auto mmas = [&](const u32x4 (&af)[TQ], const u32x4 (&xf)[MS]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int m = 0; m < MS; ++m)
+#pragma unroll
+                for (int q = 0; q < TQ; ++q) acc[m][q] = Fmt::mma32(af[q], xf[m], acc[m][q]);
+        };
+        if (wn < NT) {                        // a wave without a rank tile has no MFMA work
+            // K steps of this wave: pass * ksf + s = wk (mod WK), so that the
+            // waves that split K share every pass's steps in turn
+            int s = ((wk - pass * ksf) % WK + WK) % WK;
+            for (; s + WK < ks; s += 2 * WK) {
+                u32x4 af[2][TQ], xf[2][MS];
+                frags(s, af[0], xf[0]);
+                frags(s + WK, af[1], xf[1]);
+                lgkm_wait(af[0]);
+                lgkm_wait(af[1]);
+                mask_a(af[0]);
+                mask_a(af[1]);
+                mmas(af[0], xf[0]);
+                mmas(af[1], xf[1]);
+            }
+            if (s < ks) {
+                u32x4 af[TQ], xf[MS];
+                frags(s, af, xf);
+                lgkm_wait(af);
+                mask_a(af);
+                mmas(af, xf);
+            }
+        }
+    }
+
+    // lane holds v[row m*16+lr][ranks tile*16 + 4lg .. +3]; the partial block
+    // is [nrows][R]
+    const float* pbase = a.partials + it.part + (kSync && parity ? a.pbuf : 0);
+    const rsrc_t pr = make_rsrc(pbase, (uint32_t)it.pstride * 4);
+    if (WK == 1) {
+#pragma unroll
+        for (int m = 0; m < MS; ++m) {
+#pragma unroll
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                const int row = m * 16 + lr;
+                const int r0 = tile * 16 + 4 * lg;
+                const bool ok = tile < NT && row < nrows && r0 < R;
+                if constexpr (kSync) sync_store16(as_u4(acc[m][q]), pr, ok ? (row * R + r0) * 4 : kOut);
+                else bstore16(as_u4(acc[m][q]), pr, ok ? (row * R + r0) * 4 : kOut);
+            }
+        }
+    } else {
+        __syncthreads();                      // the buffers are read no more
+        float* red = (float*)smem;            // [WK][MS*16][Rp + 4]
+        const int RS = Rp + 4;
+#pragma unroll
+        for (int m = 0; m < MS; ++m) {
+#pragma unroll
+            for (int q = 0; q < TQ; ++q) {
+                const int tile = wn + WN * q;
+                if (tile < NT)
+                    *(f32x4*)(red + ((wk * MS + m) * 16 + lr) * RS + tile * 16 + 4 * lg) = acc[m][q];
+            }
+        }
+        __syncthreads();
+        const int n4 = nrows * R / 4;
+        for (int o = t; o < n4; o += kThreads) {
+            const int row = (4 * o) / R;
+            const int r0 = 4 * o - row * R;
+            f32x4 sum = *(const f32x4*)(red + row * RS + r0);
+            for (int k = 1; k < WK; ++k) sum += *(const f32x4*)(red + (k * MS * 16 + row) * RS + r0);
+            if constexpr (kSync) sync_store16(as_u4(sum), pr, 16 * o);
+            else bstore16(as_u4(sum), pr, 16 * o);
+        }
+    }
+    if constexpr (kSync) {
+        // arm this block in the other buffer for the next launch (plain
+        // stores: only the next launch reads them)
+        const rsrc_t orr = make_rsrc(a.partials + it.part + (parity ? 0 : a.pbuf), (uint32_t)it.pstride * 4);
+        const u32x4 s4 = {kSentinel, kSentinel, kSentinel, kSentinel};
+        for (int o = t; 4 * o < it.pstride; o += kThreads) bstore16(s4, orr, 16 * o);
+    }
+}
+
 template <class Fmt, bool kSync>
 __device__ __forceinline__ void shrink_item(const KernelArgs& a, const Item& it, unsigned char* smem) {
     const int tq = shrink_tq(it.rank, it.nrows);
     const int ms = msub_body(it.nrows);
+    if (shrink_uses_dma(it.rank, it.nrows)) {     // ms is 2 or 4
+        if (tq == 1) {
+            if (ms == 2) shrink_dma_body<Fmt, 1, 2, kSync>(a, it, smem);
+            else shrink_dma_body<Fmt, 1, 4, kSync>(a, it, smem);
+        } else if (tq == 2) {
+            if (ms == 2) shrink_dma_body<Fmt, 2, 2, kSync>(a, it, smem);
+            else shrink_dma_body<Fmt, 2, 4, kSync>(a, it, smem);
+        } else {
+            if (ms == 2) shrink_dma_body<Fmt, 4, 2, kSync>(a, it, smem);
+            else shrink_dma_body<Fmt, 4, 4, kSync>(a, it, smem);
+        }
+        return;
+    }
     if (tq == 1) {
         if (ms == 1) shrink_body<Fmt, 1, 1, kSync>(a, it, smem);
         else if (ms == 2) shrink_body<Fmt, 1, 2, kSync>(a, it, smem);
@@ -625,7 +912,9 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     const int R = it.rank;
     const int Rv = rank_stride(R);
     const int KS = round_up_i(R, 16) / 16;
-    const int len = it.len;
+    const int len = it.len;                   // columns of the item: one tile, or (prompt items) several
+    constexpr int kTile = 256 * Q;            // columns of a tile
+    int tl = 0;                               // the current tile's first column within the item
     const int nrows = it.nrows;
     const int h_out = kMulti ? it.h_out : a.h_out;
     u32x4* Vf = (u32x4*)smem;                 // [MS][KS][64] operand fragments of v
@@ -644,18 +933,25 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     constexpr int YS = kStage ? MS * 16 * TC / kThreads : 1;
     int yoff[kStage ? 1 : Q][MS][2];
     u32x4 yv[kStage ? 1 : Q][MS][2];
+    // Larger items: the tile's y goes straight into LDS (buffer-to-LDS loads),
+    // row r's chunk c at slot r TC + (c ^ (r % 8)); thread t moves slots
+    // t + 256 i, wave w's load i slots 256 i + 64 w .. + 63.
+    unsigned char* Ysb = smem + kExpandYsOff;
     int soff[YS];
-    u32x4 ys[YS];
-    if constexpr (kStage) {
+    auto y_tile = [&]() __attribute__((always_inline)) {
+        const int wu = __builtin_amdgcn_readfirstlane(w);
 #pragma unroll
         for (int i = 0; i < YS; ++i) {
             const int p = t + i * kThreads;
             const int r = p / TC;
-            const int c = p - r * TC;
+            const int c = (p - r * TC) ^ (r & 7);
             const int row = row_of(rowv, r < nrows ? r : 0);
-            soff[i] = r < nrows && 8 * c + 8 <= len ? (int)(((int64_t)row * ldy + it.lo + 8 * c) * 2) : kOut;
-            ys[i] = bload16(yr, soff[i]);
+            soff[i] = r < nrows && tl + 8 * c + 8 <= len ? (int)(((int64_t)row * ldy + it.lo + tl + 8 * c) * 2) : kOut;
+            dma16(yr, Ysb + (i * kThreads + 64 * wu) * 16, soff[i]);
         }
+    };
+    if constexpr (kStage) {
+        y_tile();
     } else {
 #pragma unroll
         for (int m = 0; m < MS; ++m) {
@@ -696,8 +992,8 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             const int j0 = 16 * (g0 + kl) + 8 * (lg & 1);
 #pragma unroll
             for (int kk = 0; kk < 8; ++kk) {
-                const bool ok = j0 + kk < R && col + 4 <= len;
-                bv[p][kk] = bload8(br, ok ? ((j0 + kk) * h_out + col) * 2 : kOut);
+                const bool ok = j0 + kk < R && tl + col + 4 <= len;
+                bv[p][kk] = bload8(br, ok ? ((j0 + kk) * h_out + tl + col) * 2 : kOut);
             }
         }
     };
@@ -820,7 +1116,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     // decode items (one subtile) put the next rank group's B in flight from
     // here, during the barrier and this group's MFMAs (larger items, whose B
     // mostly comes from L2, keep the registers for their accumulators)
-    constexpr bool kAhead = MS == 1;
+    constexpr bool kAhead = MS != 2;          // (items of two subtiles: registers)
     if (kAhead && KSG < KS) load_group(KSG);
     __syncthreads();
     float escale = it.scale;                  // s_g, times 2^-k when v was scaled
@@ -840,7 +1136,15 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             (void)__builtin_amdgcn_atomic_inc32(a.sync + (int64_t)it.rb * kSyncStride, 2u * (uint32_t)it.nexp - 1u,
                                                 __ATOMIC_RELAXED, "agent");
 
-    // --- y^T = B^T v^T on MFMA (16x16x32: 16 ranks x high and low part of v)
+    // --- per tile: y^T = B^T v^T on MFMA (16x16x32: 16 ranks x high and low
+    // part of v), then the epilogue.  A prompt item walks its tiles with the
+    // v fragments made once; the next tile's B and y are loaded while this
+    // tile's epilogue runs.
+    for (;;) {
+    if (tl > 0) {                             // a later tile: its group 0 was loaded in the last epilogue
+        prepare();
+        if (kAhead && KSG < KS) load_group(KSG);
+    }
     f32x4 acc[Q][4][MS];
 #pragma unroll
     for (int q = 0; q < Q; ++q)
@@ -880,18 +1184,19 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         }
     }
 
+    const bool more = MS == 4 && tl + kTile < len;  // the item has another tile
+
     // --- epilogue: lane holds, for instruction c and output row 4lg + i,
     // column cb*64 + 8lg + 32(i >> 1) + 4(i & 1) + c of row m*16 + lr
-    u32x4* Ys = (u32x4*)smem;                 // staged y: [MS*16][TC + 1] chunks (odd stride)
+    u32x4* Ys = (u32x4*)Ysb;
     if constexpr (kStage) {
-        __syncthreads();                      // every wave's reads of the v fragments are done
-#pragma unroll
-        for (int i = 0; i < YS; ++i) {
-            const int p = t + i * kThreads;
-            const int r = p / TC;
-            Ys[r * (TC + 1) + (p - r * TC)] = ys[i];
+        wait_vm<0>();                         // this thread's y loads have landed (and anything before them)
+        stage_barrier();                      // every thread's have
+        if (more) {                           // the next tile's B, during this epilogue
+            tl += kTile;
+            load_group(0);
+            tl -= kTile;
         }
-        __syncthreads();
     }
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -899,7 +1204,8 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         for (int m = 0; m < MS; ++m) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int sidx = (m * 16 + lr) * (TC + 1) + (w + 4 * q) * 8 + 4 * h + lg;
+                const int yr_ = m * 16 + lr;
+                const int sidx = yr_ * TC + (((w + 4 * q) * 8 + 4 * h + lg) ^ (yr_ & 7));
                 u32x4 yo;
                 if constexpr (kStage) yo = Ys[sidx];
                 else yo = yv[q][m][h];
@@ -921,11 +1227,12 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
     if constexpr (kStage) {
         __syncthreads();
 #pragma unroll
-        for (int i = 0; i < YS; ++i) {
-            const int p = t + i * kThreads;
-            const int r = p / TC;
-            bstore16(Ys[r * (TC + 1) + (p - r * TC)], yr, soff[i]);
-        }
+        for (int i = 0; i < YS; ++i) bstore16(Ys[t + i * kThreads], yr, soff[i]);
+    }
+    if (!more) break;
+    tl += kTile;
+    __syncthreads();                          // every thread has read Ys for its stores
+    y_tile();                                 // the next tile's y, during its MFMAs
     }
 }
 
@@ -953,8 +1260,7 @@ __device__ __forceinline__ void expand_item(const KernelArgs& a, const Item& it,
         }
     } else {
         if (ksg == 1) expand_body<Fmt, 1, 1, 4, kSync, kMulti>(a, it, smem);
-        else if (ksg == 2) expand_body<Fmt, 1, 2, 4, kSync, kMulti>(a, it, smem);
-        else expand_body<Fmt, 1, 4, 4, kSync, kMulti>(a, it, smem);
+        else expand_body<Fmt, 1, 2, 4, kSync, kMulti>(a, it, smem);   // ksg <= 2 with four subtiles
     }
 }
 
