@@ -11,9 +11,9 @@
 // the MFMA ridge, so the tile runs at MFMA rate while the delta costs r_g/K of
 // the base work.
 //
-// Tile: 256 rows of x (tokens) x 256 columns of y, one workgroup of 8 wave64
-// (2 x 4 waves, each 128 rows x 64 columns of the tile: 4 x 2 MFMA blocks of
-// 32 x 32, 128 float32 accumulators per lane).  The contraction runs on
+// Tile: 256 rows of x (tokens) x 256 columns of y, one workgroup of 4 wave64
+// (2 x 2 waves, each 128 rows x 128 columns of the tile: 4 x 4 MFMA blocks of
+// 32 x 32, 256 float32 accumulators per lane, one wave per SIMD).  The contraction runs on
 // v_mfma_f32_32x32x16 (measured here: about 34 cycles for its 32768 flop with
 // four independent accumulators, against about 27 for the 16384 of a
 // 16x16x32 even with sixteen) with the base weight as the A operand (rows =
@@ -29,9 +29,9 @@
 // one whole 128-byte line: eight consecutive lanes load one row slice
 // (16 bytes each), a wave eight whole rows per instruction.  (Loads of 32
 // bytes per row from 32 rows, in the operand's own order, measured about
-// 9 bytes per cycle per CU and bounded the kernel.)  The stage is loaded into
-// registers one step ahead and written to the other of two 64 KiB LDS
-// buffers in the order the MFMA operands are read: per 32-row block and
+// 9 bytes per cycle per CU and bounded the kernel.)  Each stage is loaded
+// into registers two steps ahead and written, one step ahead, to the other
+// of two 64 KiB LDS buffers in the order the MFMA operands are read: per 32-row block and
 // K-16 slice a 1 KiB region holding chunk c of row r at 32 (c % 2) + r % 32,
 // so the 64 lanes of an operand read one contiguous KiB, free of bank
 // conflicts.  Rows past the batch, columns past h_out and K past h_in are
@@ -52,6 +52,13 @@
 // (p / n_xcd)-th tile of that XCD's contiguous share of the row-major tile
 // order, so the tiles an XCD runs at a time share rows of x and columns of W
 // in its L2.
+//
+// A last round of tiles that would leave compute units idle is split along
+// K: each of its tiles runs as `split` workgroups over consecutive K ranges,
+// which store their float32 partial tiles (in accumulator order, the first
+// range with the adapter delta added) to the workspace; the reduction kernel
+// adds a tile's ranges in order 0, 1, ..., rounds once and stores y, so the
+// result does not depend on timing.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 

@@ -950,8 +950,11 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
             dma16(yr, Ysb + (i * kThreads + 64 * wu) * 16, soff[i]);
         }
     };
-    if constexpr (kStage) {
-        y_tile();
+    if constexpr (kStage && kSync) {
+        y_tile();                             // in flight while the item waits for its v
+    } else if constexpr (kStage) {
+        // separate launch (v is ready): y after the v loads, so that those
+        // are not queued behind it
     } else {
 #pragma unroll
         for (int m = 0; m < MS; ++m) {
@@ -1106,6 +1109,7 @@ __device__ __forceinline__ void expand_body(const KernelArgs& a, const Item& it,
         }
     };
     fill(std::false_type{}, 1.f);
+    if constexpr (kStage && !kSync) y_tile();
     float* vmax = (float*)(smem + kExpandVmaxOff);   // one float per wave
     if constexpr (Fmt::kNarrowRange) {
 #pragma unroll
