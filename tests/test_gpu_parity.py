@@ -148,6 +148,10 @@ SELECTOR_CASES = [
      [0, 1, -1, 2, 3, 4, 5, 1]),
     (W.F16, 520, 2056, [3, 24, 1, 200, 255], [2, 1, 7, 1, 9], [0, 1, 2, 3, 4]),
     (W.BF16, 8192, 8200, [64, 16], [300, 1, 1, 77], [0, 1, -1, 0]),
+    # prompt-sized blocks through LDS at every A row width (1, 3, 4, 6, 16
+    # and 24 chunks), blocks of two and four subtiles, a last pass of 40 K
+    # and a last column tile of 16 columns
+    (W.BF16, 1064, 1040, [8, 24, 32, 48, 128, 192], [20, 70, 130, 33, 17, 64], [0, 1, 2, 3, 4, 5]),
 ]
 
 
@@ -194,6 +198,7 @@ RANDOM_CASES = [
     (3, W.F16, 776, 520, 4, [3, 40, 96, 1], [1, 5, 1, 2, 1, 33], "uniform"),
     (4, W.BF16, 5120, 13824, 8, [8, 16, 32, 64], [1] * 20, "zipf"),
     (5, W.BF16, 13824, 5120, 8, [8, 16, 32, 64], [1] * 20, "zipf"),
+    (6, W.F16, 1064, 1040, 6, [8, 24, 32, 48, 128, 192], [20, 70, 1, 130, 33, 17, 64, 3], "uniform"),
 ]
 
 
@@ -256,6 +261,8 @@ def test_random_parity_fused_shrink_expand(case):
     L.lora_expand(p.table, dw.batch, v, ldv, y2, y2.shape[1], ws, n, stream())
     torch.cuda.synchronize()
     assert np.array_equal(D.from_device_bits(y2), got)
+    # the one-launch step == the separate launches, bit for bit
+    assert np.array_equal(run_plan(dw, "proj"), got)
     dw.release()
 
 
