@@ -492,6 +492,15 @@ def test_edge_cases():
                             w.ranks, w.scales, w.projections[0].y[:1], w.dtype)
     compare(D.from_device_bits(y), ref, w.dtype, "single row")
     dw.release()
+    # 8-wide projections with prompt-sized blocks: a single partial pass of
+    # the LDS-staged shrink, a single partial column tile of the expand
+    wt = W.small_random(77, dtype=W.BF16, h_in=8, h_out=8, n_adapters=3, rank_set=[8, 16, 256],
+                        seg_lens=[70, 33, 5, 40], seg_adapter=np.array([0, 1, 2, 1], np.int32))
+    dwt = D.upload(wt, DEV)
+    got = run_fused(dwt, "proj")
+    compare(got, oracle_full(wt, "proj"), wt.dtype, "h = 8")
+    assert np.array_equal(run_plan(dwt, "proj"), got)
+    dwt.release()
 
 
 def test_errors_are_reported_not_enqueued():
