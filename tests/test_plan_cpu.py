@@ -36,6 +36,45 @@ def partitions(ranges, total):
     return at == total
 
 
+STAGE_CHUNKS = 1024            # 16-byte chunks of one LDS buffer of the LDS-staged shrink
+SHRINK_LDS = 4 * STAGE_CHUNKS * 16
+EXPAND_YS_OFF = 32 * 1024       # expand: v fragments below, the staged y tile above
+EXPAND_VMAX_OFF = EXPAND_YS_OFF + 33 * 1024 + 256 - 16
+
+
+def ceil_to(v, m):
+    return (v + m - 1) // m * m
+
+
+def check_lds_fit(rank, nrows, sh, ex):
+    """Every item's staging fits the LDS its kernel body lays out: a shrink
+    pass of a block of more than 16 rows (rank a multiple of 8) in one
+    16 KiB buffer of the LDS-staged body (A rows rounded to whole 1 KiB wave
+    loads, then the x rows), other passes in the register-staged body's
+    space; an expand item's v fragments below the y tile, its y tile (and
+    the columns it walks) within the rest."""
+    ms = 1 if nrows <= 16 else (2 if nrows <= 32 else 4)
+    rp = ceil_to(rank, 16)
+    for sub in set(sh["sub"].tolist()):
+        stage = ceil_to(sub * (rank // 8), 64) + 2 * ms * sub
+        if ms > 1 and rank % 8 == 0 and stage <= STAGE_CHUNKS:
+            assert sub % 32 == 0 and (sub % 64 == 0 or sub == 32) and sub <= 512
+        else:
+            wn = 4 if ms == 1 else (4 if rp // 16 >= 4 else (2 if rp // 16 >= 2 else 1))
+            staged = (rp + ms * 16) * (sub // 8 + 1) * 16
+            red = (4 // wn) * ms * 16 * (rp + 4) * 4 if wn < 4 else 0
+            assert max(staged, red) <= SHRINK_LDS, (rank, nrows, sub)
+    q = 32768 // (rp * 512)
+    q = 4 if q >= 4 else (2 if q >= 2 else 1)
+    while q * ms > 4:
+        q //= 2
+    tiles = 2 if ms == 4 else 1
+    assert np.all(ex["len"] <= 256 * q * tiles), (rank, nrows)
+    assert ms * (rp // 16) * 64 * 16 <= EXPAND_YS_OFF
+    if ms > 1:
+        assert EXPAND_YS_OFF + ms * 16 * (32 * q + 1) * 16 <= EXPAND_VMAX_OFF
+
+
 def check_plan(items, h_in, h_out, n_xcd):
     grid = items[items["grid_pos"] >= 0]
     extra = items[items["grid_pos"] < 0]
@@ -59,6 +98,7 @@ def check_plan(items, h_in, h_out, n_xcd):
         assert np.all(sh["sub"] % 32 == 0) and np.all(sh["len"] % 8 == 0)
         assert len(ex) >= 1 and partitions(zip(ex["lo"], ex["len"]), h_out)
         assert np.all(ex["len"] % 8 == 0)
+        check_lds_fit(rank, nrows, sh, ex)
         assert partitions(zip(allrd["lo"], allrd["len"]), pstride)
         direct = set(ex["sub"].tolist())
         assert len(direct) == 1
@@ -123,6 +163,17 @@ def test_decode_headline_is_laid_out_and_few_adapters_are_not():
     items = L.lora_plan_inspect(b, 4096, 4096, [64], n_xcd=8)
     assert not (items[items["grid_pos"] >= 0]["kind"] == 0).any()
     check_plan(items, 4096, 4096, 8)
+
+
+@pytest.mark.parametrize("name", ["prefill", "llama70b_mixed", "llama13b_layer"])
+def test_named_workload_plans(name):
+    """The benchmark's prompt-sized and mixed batches: forward progress,
+    exact coverage and LDS fit of every item, for every projection."""
+    from paper_2401_11240_amd import workloads as W
+    w = W.NAMED[name]()
+    for p in w.projections:
+        items = L.lora_plan_inspect(L.Batch(w.seg_offset, w.seg_adapter), p.h_in, p.h_out, w.ranks, n_xcd=8)
+        check_plan(items, p.h_in, p.h_out, 8)
 
 
 def test_inspect_errors():
