@@ -165,7 +165,7 @@ def test_decode_headline_is_laid_out_and_few_adapters_are_not():
     check_plan(items, 4096, 4096, 8)
 
 
-@pytest.mark.parametrize("name", ["prefill", "llama70b_mixed", "llama13b_layer"])
+@pytest.mark.parametrize("name", ["prefill", "llama13b_layer"])
 def test_named_workload_plans(name):
     """The benchmark's prompt-sized and mixed batches: forward progress,
     exact coverage and LDS fit of every item, for every projection."""
