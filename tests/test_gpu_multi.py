@@ -117,6 +117,17 @@ def test_13b_layer_shared_inputs_in_one_launch():
     check_workload(W.NAMED["llama13b_layer"]())
 
 
+def test_more_than_128_distinct_adapters_in_one_launch():
+    # every projection's factor pointers come from its table (the launch's
+    # pointer table is the projections' tables, not 128 kernel-argument slots)
+    w = W.build_workload(name="multi_pool", seed=41, dtype=W.BF16, n_adapters=400, rank_set=[8, 16, 32, 64],
+                         adapter_law="uniform", n_segments=202, seg_lens=[1] * 200 + [40, 70],
+                         projections=(("q", 1024, 1024, "x"), ("gate", 1024, 2056, "x")))
+    ra = w.row_adapter()
+    assert np.unique(ra[ra >= 0]).size > 128
+    check_workload(w, graph_replays=1, against_oracle=True)
+
+
 def test_70b_batch_q_and_gate_in_one_launch():
     check_workload(W.NAMED["llama70b_mixed"](), graph_replays=1)
 
