@@ -491,7 +491,8 @@ def measure_coldstart(torch, dev, layers: int = 8, tokens: int = 1024, reps: int
             kw = {}
             if mode == "assist_profiled":
                 # the profile: the CPU path's time per layer and the load's rate, both measured above
-                kw = dict(cpu_layer_ms=res["cpu"]["ms"] / layers, load_gbps=out["adapter_load"]["GBps"])
+                kw = dict(cpu_layer_ms=res["cpu"]["ms"] / layers, load_gbps=out["adapter_load"]["GBps"],
+                          gpu_layer_ms=res["gpu"]["ms"] / layers)
             for _ in range(reps):
                 r = P.run(s, mode=mode.split("_")[0], side_stream=side, ballast=ballast, **kw)
                 ms.append(r.ms)

@@ -234,7 +234,7 @@ class ColdStartPrompt:
         return self.seq_load
 
     def run(self, stream, mode: str = "assist", side_stream=None, ballast=None, cpu_layer_ms: float = None,
-            load_gbps: float = None) -> PromptResult:
+            load_gbps: float = None, gpu_layer_ms: float = None) -> PromptResult:
         """mode: "assist" (CPU until the load lands, then GPU), "cpu" (every
         layer on the CPU path), "gpu" (adapter already resident), "wait"
         (load, wait for it, then every layer on the GPU: on-demand loading).
@@ -243,7 +243,9 @@ class ColdStartPrompt:
         load_gbps, the host -> device rate), "assist" starts a CPU layer only
         while the load's predicted remaining time exceeds it, and otherwise
         waits for the load: a CPU layer that would end after the adapter lands
-        only delays the GPU's take-over."""
+        only delays the GPU's take-over.  With gpu_layer_ms too, it stays on
+        the CPU for every remaining layer when that ends no later than
+        waiting for the load and running them on the GPU."""
         torch = self.torch
         res = PromptResult()
         t0 = time.perf_counter()
@@ -259,7 +261,10 @@ class ColdStartPrompt:
                 landed = flag_test(self.flags.addr(0), target)
                 if not landed and cpu_layer_ms and load_gbps:
                     left_ms = self.load_bytes / (load_gbps * 1e6) - (time.perf_counter() - self.load_started) * 1e3
-                    if left_ms < cpu_layer_ms:
+                    remaining = len(self.layers) - li
+                    stay = gpu_layer_ms is not None and \
+                        remaining * cpu_layer_ms <= max(left_ms, 0.0) + remaining * gpu_layer_ms
+                    if not stay and left_ms < cpu_layer_ms:
                         flag_wait(self.flags.addr(0), target)
                         landed = True
                 if landed:

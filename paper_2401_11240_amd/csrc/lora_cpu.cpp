@@ -2,7 +2,10 @@
 // parallelization"): the delta s ((x A) B) of a prompt's rows on host cores,
 // the rows split into token slices, one thread per slice.  float32
 // arithmetic, AVX2/FMA code paths (every x86-64 server core this library
-// targets has them).
+// targets has them), with 32-column AVX-512F tiles where the host has them
+// (the same fused multiply-adds in the same order: the same bits).  The
+// factors are widened to float32 once per call, in parallel, B into blocks
+// of columns so that a block's rank rows are contiguous.
 #include <immintrin.h>
 
 #include <algorithm>
@@ -22,6 +25,56 @@
 namespace lora {
 int set_error(int code, const std::string& msg);
 }
+
+namespace {
+
+// C[i][0..32) (+)= sum_k X_i[k] Y[k][0..32) for four rows: the 4 x 32 tile of
+// eight 16-wide accumulators (AVX-512F), each sum in k order with fused
+// multiply-adds, as the 4 x 16 tile below, so the two give the same bits.
+template <bool ACC>
+__attribute__((target("avx512f"))) inline void tile4x32(const float* const X[4], const float* Y, int64_t ldy,
+                                                        int32_t K, float* const C[4]) {
+    __m512 c00, c01, c10, c11, c20, c21, c30, c31;
+    if (ACC) {
+        c00 = _mm512_loadu_ps(C[0]), c01 = _mm512_loadu_ps(C[0] + 16), c10 = _mm512_loadu_ps(C[1]);
+        c11 = _mm512_loadu_ps(C[1] + 16), c20 = _mm512_loadu_ps(C[2]), c21 = _mm512_loadu_ps(C[2] + 16);
+        c30 = _mm512_loadu_ps(C[3]), c31 = _mm512_loadu_ps(C[3] + 16);
+    } else {
+        c00 = c01 = c10 = c11 = c20 = c21 = c30 = c31 = _mm512_setzero_ps();
+    }
+    for (int32_t k = 0; k < K; ++k) {
+        const float* y = Y + (int64_t)k * ldy;
+        const __m512 y0 = _mm512_loadu_ps(y), y1 = _mm512_loadu_ps(y + 16);
+        __m512 b = _mm512_set1_ps(X[0][k]);
+        c00 = _mm512_fmadd_ps(b, y0, c00);
+        c01 = _mm512_fmadd_ps(b, y1, c01);
+        b = _mm512_set1_ps(X[1][k]);
+        c10 = _mm512_fmadd_ps(b, y0, c10);
+        c11 = _mm512_fmadd_ps(b, y1, c11);
+        b = _mm512_set1_ps(X[2][k]);
+        c20 = _mm512_fmadd_ps(b, y0, c20);
+        c21 = _mm512_fmadd_ps(b, y1, c21);
+        b = _mm512_set1_ps(X[3][k]);
+        c30 = _mm512_fmadd_ps(b, y0, c30);
+        c31 = _mm512_fmadd_ps(b, y1, c31);
+    }
+    _mm512_storeu_ps(C[0], c00);
+    _mm512_storeu_ps(C[0] + 16, c01);
+    _mm512_storeu_ps(C[1], c10);
+    _mm512_storeu_ps(C[1] + 16, c11);
+    _mm512_storeu_ps(C[2], c20);
+    _mm512_storeu_ps(C[2] + 16, c21);
+    _mm512_storeu_ps(C[3], c30);
+    _mm512_storeu_ps(C[3] + 16, c31);
+}
+
+// AVX-512F on this host (decided once)
+bool wide_tiles() {
+    static const bool on = __builtin_cpu_supports("avx512f");
+    return on;
+}
+
+}  // namespace
 
 #pragma clang attribute push(__attribute__((target("avx2,fma,f16c"))), apply_to = function)
 
@@ -46,16 +99,34 @@ void widen(const uint16_t* src, float* dst, int64_t n, int32_t dtype) {
     }
 }
 
+struct Job;
+typedef void (*TaskFn)(const Job&, int32_t);
+
 struct Job {
     const uint16_t* x;
     int64_t ldx;
     int32_t h_in, h_out, rank, dtype;
     const float* A;        // [h_in, rank]
-    const float* B;        // [rank, h_out]
+    const float* B;        // column blocks of B: block b is [rank][nbw] (columns b nbw .., zeros past h_out)
+    int32_t nbw;           // columns per block
     float scale;
     float* delta;
     int64_t ld_delta;
+    // the pool's work: task(job, i) for i < n_tasks
+    TaskFn task;
+    int32_t n_tasks, chunk, n_rows;
+    // widening of the factors (16-bit input, float32 copies)
+    const uint16_t* A16;
+    const uint16_t* B16;
+    int64_t widen_per_task;
 };
+
+// Grow-only float buffers, kept across calls (each thread its own): fresh
+// pages for every call cost more than a short prompt's arithmetic.
+float* scratch(std::vector<float>& v, size_t n) {
+    if (v.size() < n) v.resize(n);
+    return v.data();
+}
 
 constexpr int32_t kKChunk = 128;   // rows of A kept in L1 while every row of a slice runs over them
 
@@ -104,13 +175,22 @@ inline void tile4x16(const float* const X[4], const float* Y, int64_t ldy, int32
 template <bool ACC>
 void block_product(const float* const X[4], int nt, const float* Y, int64_t ldy, int32_t K, int32_t N,
                    float* const C[4]) {
-    float scratch[4][16];
+    float scratch[4][32];
     int32_t n = 0;
+    if (wide_tiles())
+        for (; n + 32 <= N; n += 32) {
+            float* dst[4];
+            for (int i = 0; i < 4; ++i) {
+                dst[i] = i < nt ? C[i] + n : scratch[i];
+                if (ACC && i >= nt) std::memcpy(scratch[i], C[nt - 1] + n, 32 * sizeof(float));
+            }
+            tile4x32<ACC>(X, Y + n, ldy, K, dst);
+        }
     for (; n + 16 <= N; n += 16) {
         float* dst[4];
         for (int i = 0; i < 4; ++i) {
             dst[i] = i < nt ? C[i] + n : scratch[i];
-            if (ACC && i >= nt) std::memcpy(scratch[i], C[nt - 1] + n, sizeof scratch[i]);
+            if (ACC && i >= nt) std::memcpy(scratch[i], C[nt - 1] + n, 16 * sizeof(float));
         }
         tile4x16<ACC>(X, Y + n, ldy, K, dst);
     }
@@ -127,8 +207,11 @@ void block_product(const float* const X[4], int nt, const float* Y, int64_t ldy,
 // one 16-column block of B at a time (the block stays in L1 across the rows)
 void run_rows(const Job& J, int32_t t0, int32_t t1) {
     const int32_t R = J.rank, n = t1 - t0;
-    std::vector<float> xr((size_t)n * J.h_in), v((size_t)n * R, 0.f);
-    for (int32_t i = 0; i < n; ++i) widen(J.x + (int64_t)(t0 + i) * J.ldx, xr.data() + (size_t)i * J.h_in, J.h_in, J.dtype);
+    static thread_local std::vector<float> xbuf, vbuf;
+    float* const xr = scratch(xbuf, (size_t)n * J.h_in);
+    float* const vr = scratch(vbuf, (size_t)n * R);
+    std::fill(vr, vr + (size_t)n * R, 0.f);
+    for (int32_t i = 0; i < n; ++i) widen(J.x + (int64_t)(t0 + i) * J.ldx, xr + (size_t)i * J.h_in, J.h_in, J.dtype);
     auto rows = [&](int32_t tb, int nt, const float* base, size_t ld, int64_t off, const float* P[4]) {
         for (int i = 0; i < 4; ++i) P[i] = base + (size_t)(tb + std::min(i, nt - 1)) * ld + off;
     };
@@ -137,23 +220,53 @@ void run_rows(const Job& J, int32_t t0, int32_t t1) {
         for (int32_t tb = 0; tb < n; tb += 4) {
             const int nt = std::min<int32_t>(4, n - tb);
             const float* X[4];
-            rows(tb, nt, xr.data(), J.h_in, k0, X);
+            rows(tb, nt, xr, J.h_in, k0, X);
             float* V[4];
-            for (int i = 0; i < 4; ++i) V[i] = v.data() + (size_t)(tb + std::min(i, nt - 1)) * R;
+            for (int i = 0; i < 4; ++i) V[i] = vr + (size_t)(tb + std::min(i, nt - 1)) * R;
             block_product<true>(X, nt, J.A + (int64_t)k0 * R, R, kc, R, V);
         }
     }
-    for (float& e : v) e *= J.scale;
-    for (int32_t n0 = 0; n0 < J.h_out; n0 += 16) {
-        const int32_t nc = std::min<int32_t>(16, J.h_out - n0);
+    for (size_t i = 0; i < (size_t)n * R; ++i) vr[i] *= J.scale;
+    const int32_t nb = J.nbw;                // one block of B at a time (it stays in L1)
+    for (int32_t n0 = 0; n0 < J.h_out; n0 += nb) {
+        const int32_t nc = std::min<int32_t>(nb, J.h_out - n0);
         for (int32_t tb = 0; tb < n; tb += 4) {
             const int nt = std::min<int32_t>(4, n - tb);
             const float* Vr[4];
-            rows(tb, nt, v.data(), R, 0, Vr);
+            rows(tb, nt, vr, R, 0, Vr);
             float* O[4];
             for (int i = 0; i < 4; ++i) O[i] = J.delta + (int64_t)(t0 + tb + std::min(i, nt - 1)) * J.ld_delta + n0;
-            block_product<false>(Vr, nt, J.B + n0, J.h_out, R, nc, O);
+            block_product<false>(Vr, nt, J.B + (size_t)(n0 / nb) * R * nb, nb, R, nc, O);
         }
+    }
+}
+
+// B's rank rows [k0, k1) into the column blocks
+void widen_b_rows(const Job& J, int32_t k0, int32_t k1) {
+    const int32_t nbw = J.nbw, nblk = (J.h_out + nbw - 1) / nbw;
+    float* const Bp = const_cast<float*>(J.B);
+    for (int32_t k = k0; k < k1; ++k)
+        for (int32_t b = 0; b < nblk; ++b) {
+            const int32_t n0 = b * nbw, nc = std::min(nbw, J.h_out - n0);
+            float* dst = Bp + ((size_t)b * J.rank + k) * nbw;
+            widen(J.B16 + (int64_t)k * J.h_out + n0, dst, nc, J.dtype);
+            for (int32_t j = nc; j < nbw; ++j) dst[j] = 0.f;
+        }
+}
+
+// pool tasks: slice i of the rows; part i of the factors' widening (the
+// first half of the tasks A's elements, the second half B's rank rows)
+void rows_task(const Job& J, int32_t i) { run_rows(J, i * J.chunk, std::min(J.n_rows, (i + 1) * J.chunk)); }
+void widen_task(const Job& J, int32_t i) {
+    const int32_t half = J.n_tasks / 2;
+    if (i < half) {
+        const int64_t na = (int64_t)J.h_in * J.rank;
+        const int64_t lo = i * J.widen_per_task, hi = std::min(na, lo + J.widen_per_task);
+        if (lo < hi) widen(J.A16 + lo, const_cast<float*>(J.A) + lo, hi - lo, J.dtype);
+    } else {
+        const int32_t per = (J.rank + (J.n_tasks - half) - 1) / (J.n_tasks - half);
+        const int32_t k0 = (i - half) * per;
+        widen_b_rows(J, std::min(k0, J.rank), std::min(J.rank, k0 + per));
     }
 }
 
@@ -175,19 +288,18 @@ struct Pool {
     std::condition_variable cv_work, cv_done;
     std::vector<std::thread> workers;
     const Job* job = nullptr;
-    int32_t c = 0, n_rows = 0, n_slices = 0;
     std::atomic<int32_t> next{0};
-    int32_t done = 0;                   // slices finished in this call
+    int32_t done = 0;                   // tasks finished in this run
     int32_t active = 0;                 // workers between taking the job and reporting back
     uint64_t gen = 0;
 
-    // slices until none is left; returns how many this thread ran
-    int32_t drain(const Job& J, int32_t cc, int32_t rows, int32_t slices) {
+    // tasks until none is left; returns how many this thread ran
+    int32_t drain(const Job& J) {
         int32_t ran = 0;
         for (;;) {
             const int32_t i = next.fetch_add(1);
-            if (i >= slices) return ran;
-            run_rows(J, i * cc, std::min(rows, (i + 1) * cc));
+            if (i >= J.n_tasks) return ran;
+            J.task(J, i);
             ++ran;
         }
     }
@@ -196,18 +308,14 @@ struct Pool {
         uint64_t seen = 0;
         for (;;) {
             const Job* J;
-            int32_t cc, rows, slices;
             {
                 std::unique_lock<std::mutex> lk(mu);
                 cv_work.wait(lk, [&] { return gen != seen && job != nullptr; });
                 seen = gen;
                 ++active;
                 J = job;
-                cc = c;
-                rows = n_rows;
-                slices = n_slices;
             }
-            const int32_t ran = drain(*J, cc, rows, slices);
+            const int32_t ran = drain(*J);
             std::lock_guard<std::mutex> lk(mu);
             done += ran;
             --active;
@@ -225,23 +333,22 @@ struct Pool {
         return true;
     }
 
-    void run(const Job& J, int32_t chunk, int32_t rows, int32_t slices) {
+    // J's tasks on the workers and the calling thread; returns when every
+    // task is done and no worker is still looking for one
+    void run(const Job& J) {
         {
             std::unique_lock<std::mutex> lk(mu);
             cv_done.wait(lk, [&] { return active == 0; });
             job = &J;
-            c = chunk;
-            n_rows = rows;
-            n_slices = slices;
             next.store(0);
             done = 0;
             ++gen;
         }
         cv_work.notify_all();
-        const int32_t ran = drain(J, chunk, rows, slices);
+        const int32_t ran = drain(J);
         std::unique_lock<std::mutex> lk(mu);
         done += ran;
-        cv_done.wait(lk, [&] { return done == n_slices && active == 0; });
+        cv_done.wait(lk, [&] { return done == J.n_tasks && active == 0; });
         job = nullptr;
     }
 };
@@ -263,10 +370,13 @@ extern "C" int lora_cpu_delta(const void* x, int64_t ldx, int32_t n_rows, int32_
     if (n_rows == 0) return LORA_OK;
     if (!x || !A || !B || !delta) return lora::set_error(LORA_E_ARG, "lora_cpu_delta: NULL argument");
     if (max_threads < 1) max_threads = 1;
-    std::vector<float> Af((size_t)h_in * rank), Bf((size_t)rank * h_out);
-    widen((const uint16_t*)A, Af.data(), (int64_t)h_in * rank, dtype);
-    widen((const uint16_t*)B, Bf.data(), (int64_t)rank * h_out, dtype);
-    const Job J{(const uint16_t*)x, ldx, h_in, h_out, rank, dtype, Af.data(), Bf.data(), scale, delta, ld_delta};
+    const int32_t nbw = wide_tiles() ? 32 : 16;
+    const int64_t na = (int64_t)h_in * rank, nb = (int64_t)rank * ((h_out + nbw - 1) / nbw) * nbw;
+    static thread_local std::vector<float> abuf, bbuf;   // the caller's; workers fill them during the call
+    float* const Af = scratch(abuf, (size_t)na);
+    float* const Bf = scratch(bbuf, (size_t)nb);
+    Job J{(const uint16_t*)x, ldx, h_in, h_out, rank, dtype, Af, Bf, nbw, scale, delta, ld_delta,
+          nullptr, 0, 0, n_rows, (const uint16_t*)A, (const uint16_t*)B, 0};
     int32_t c = tokens_per_thread > 0 ? tokens_per_thread : (n_rows + max_threads - 1) / max_threads;
     int32_t n_thr = (n_rows + c - 1) / c;
     if (n_thr > max_threads) {
@@ -274,12 +384,22 @@ extern "C" int lora_cpu_delta(const void* x, int64_t ldx, int32_t n_rows, int32_
         c = (n_rows + n_thr - 1) / n_thr;
     }
     if (n_thr <= 1) {
+        widen((const uint16_t*)A, Af, na, dtype);
+        widen_b_rows(J, 0, rank);
         run_rows(J, 0, n_rows);
         return LORA_OK;
     }
     Pool* P = pool();
     std::lock_guard<std::mutex> call(P->call_mu);
     if (!P->ensure(n_thr - 1)) return lora::set_error(LORA_E_NOMEM, "lora_cpu_delta: cannot start threads");
-    P->run(J, c, n_rows, (n_rows + c - 1) / c);
+    // the factors widened by every thread, then the row slices
+    J.task = widen_task;
+    J.n_tasks = 2 * n_thr;
+    J.widen_per_task = ((na + n_thr - 1) / n_thr + 7) / 8 * 8;
+    P->run(J);
+    J.task = rows_task;
+    J.n_tasks = (n_rows + c - 1) / c;
+    J.chunk = c;
+    P->run(J);
     return LORA_OK;
 }
