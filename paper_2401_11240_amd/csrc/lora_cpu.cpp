@@ -121,11 +121,16 @@ struct Job {
     int64_t widen_per_task;
 };
 
-// Grow-only float buffers, kept across calls (each thread its own): fresh
-// pages for every call cost more than a short prompt's arithmetic.
+// Float buffers kept across calls (each thread its own): fresh pages for
+// every call cost more than a short prompt's arithmetic.  A buffer past
+// kKeepFloats is given back after the call that needed it (release_big).
+constexpr size_t kKeepFloats = (size_t)8 << 20;   // 32 MiB
 float* scratch(std::vector<float>& v, size_t n) {
     if (v.size() < n) v.resize(n);
     return v.data();
+}
+void release_big(std::vector<float>& v) {
+    if (v.size() > kKeepFloats) std::vector<float>().swap(v);
 }
 
 constexpr int32_t kKChunk = 128;   // rows of A kept in L1 while every row of a slice runs over them
@@ -239,6 +244,8 @@ void run_rows(const Job& J, int32_t t0, int32_t t1) {
             block_product<false>(Vr, nt, J.B + (size_t)(n0 / nb) * R * nb, nb, R, nc, O);
         }
     }
+    release_big(xbuf);
+    release_big(vbuf);
 }
 
 // B's rank rows [k0, k1) into the column blocks
@@ -387,6 +394,8 @@ extern "C" int lora_cpu_delta(const void* x, int64_t ldx, int32_t n_rows, int32_
         widen((const uint16_t*)A, Af, na, dtype);
         widen_b_rows(J, 0, rank);
         run_rows(J, 0, n_rows);
+        release_big(abuf);
+        release_big(bbuf);
         return LORA_OK;
     }
     Pool* P = pool();
@@ -401,5 +410,7 @@ extern "C" int lora_cpu_delta(const void* x, int64_t ldx, int32_t n_rows, int32_
     J.n_tasks = (n_rows + c - 1) / c;
     J.chunk = c;
     P->run(J);
+    release_big(abuf);
+    release_big(bbuf);
     return LORA_OK;
 }
