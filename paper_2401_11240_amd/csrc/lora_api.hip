@@ -1075,6 +1075,7 @@ namespace {
 struct BaseLayout {
     HostPlan p;
     int ldv = 8;
+    int tile = kBaseBig;
     int n_mt = 0, n_nt = 0;
     int n_whole = 0, split = 1, chunk = 0;
     size_t off_v = 0, v_bytes = 0, off_pieces = 0, off_part = 0, part_bytes = 0, total = 0;
@@ -1087,7 +1088,8 @@ struct BaseLayout {
 // least kBaseMinSplitStages stages (an even number of them), as many as fill
 // the compute units, their partial tiles added by a second kernel.
 void choose_split(int n_tiles, int h_in, int n_cu, BaseLayout& L) {
-    const int nk = ((h_in + 2 * kBaseBK - 1) / (2 * kBaseBK)) * 2;
+    const int bk = base_bk(L.tile);
+    const int nk = ((h_in + 2 * bk - 1) / (2 * bk)) * 2;
     L.n_whole = n_tiles;
     L.split = 1;
     L.chunk = nk;
@@ -1111,8 +1113,13 @@ int build_base(const lora_table_s* t, const lora_batch_t* b, BaseLayout& L) {
     L.off_v = align_up(L.p.total_bytes);
     L.v_bytes = (size_t)b->n_rows * L.ldv * sizeof(float);
     if (L.v_bytes > kMaxSpan) return fail(LORA_E_SHAPE, "batch too large: its float32 intermediate exceeds 2 GiB");
-    L.n_mt = (b->n_rows + kBaseBM - 1) / kBaseBM;
-    L.n_nt = (t->h_out + kBaseBN - 1) / kBaseBN;
+    // the big tile while its whole tiles fill the compute units; else the
+    // small one, which has four times as many tiles to spread (a 1024-token
+    // prompt at 4096 columns: 256 whole tiles instead of 64 split four ways)
+    const int64_t big_tiles = (int64_t)((b->n_rows + kBaseBig - 1) / kBaseBig) * ((t->h_out + kBaseBig - 1) / kBaseBig);
+    L.tile = big_tiles >= t->n_cu ? kBaseBig : kBaseSmall;
+    L.n_mt = (b->n_rows + L.tile - 1) / L.tile;
+    L.n_nt = (t->h_out + L.tile - 1) / L.tile;
     // runs of rows sharing an adapter, per row tile; neighbouring segments of
     // one adapter inside a tile make one run
     std::vector<std::vector<BasePiece>> per(L.n_mt);
@@ -1122,8 +1129,8 @@ int build_base(const lora_table_s* t, const lora_batch_t* b, BaseLayout& L) {
         const int hi = b->seg_offset[sgi + 1];
         if (g < 0) continue;
         while (lo < hi) {
-            const int mt = lo / kBaseBM;
-            const int e = std::min(hi, (mt + 1) * kBaseBM);
+            const int mt = lo / L.tile;
+            const int e = std::min(hi, (mt + 1) * L.tile);
             auto& v = per[mt];
             if (!v.empty() && v.back().adapter == g && v.back().hi == lo) v.back().hi = e;
             else v.push_back(BasePiece{lo, e, g, 0});
@@ -1144,7 +1151,7 @@ int build_base(const lora_table_s* t, const lora_batch_t* b, BaseLayout& L) {
     L.off_pieces = align_up(L.off_v + L.v_bytes);
     L.off_part = align_up(L.off_pieces + std::max<size_t>(L.pieces_blob.size(), 16));
     choose_split(L.n_mt * L.n_nt, t->h_in, t->n_cu, L);
-    L.part_bytes = (size_t)(L.n_mt * L.n_nt - L.n_whole) * L.split * (kBaseBM * kBaseBN * sizeof(float));
+    L.part_bytes = (size_t)(L.n_mt * L.n_nt - L.n_whole) * L.split * ((size_t)L.tile * L.tile * sizeof(float));
     if (L.split < 2) L.part_bytes = 0;
     L.total = L.off_part + L.part_bytes;
     return LORA_OK;
@@ -1216,6 +1223,7 @@ int base_run(const lora_table_s* t, const BaseLayout& L, int n_rows, unsigned ch
     a.M = n_rows;
     a.N = t->h_out;
     a.K = t->h_in;
+    a.tile = L.tile;
     a.n_mt = L.n_mt;
     a.n_nt = L.n_nt;
     a.n_xcd = std::max(1, t->n_xcd);

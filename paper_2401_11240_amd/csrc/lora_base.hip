@@ -11,9 +11,12 @@
 // the MFMA ridge, so the tile runs at MFMA rate while the delta costs r_g/K of
 // the base work.
 //
-// Tile: 256 rows of x (tokens) x 256 columns of y, one workgroup of 4 wave64
-// (2 x 2 waves, each 128 rows x 128 columns of the tile: 4 x 4 MFMA blocks of
-// 32 x 32, 256 float32 accumulators per lane, one wave per SIMD).  The contraction runs on
+// Tile: T rows of x (tokens) x T columns of y, T = 256 or 128, one
+// workgroup of 4 wave64 (2 x 2 waves, each a T/2 x T/2 quarter of the tile:
+// (T/64)^2 MFMA blocks of 32 x 32, one wave per SIMD).  The 256 tile carries
+// 256 float32 accumulators per lane; the 128 tile serves launches whose big
+// tiles would not fill the compute units (a 1024-token prompt), which it
+// fills with whole tiles instead of K-split ones.  The contraction runs on
 // v_mfma_f32_32x32x16 (measured here: about 34 cycles for its 32768 flop with
 // four independent accumulators, against about 27 for the 16384 of a
 // 16x16x32 even with sixteen) with the base weight as the A operand (rows =
@@ -25,17 +28,20 @@
 // K in memory: every 16-byte chunk of 8 consecutive K is one MFMA operand
 // slice, with no transpose.
 //
-// Pipeline: K advances in steps of 64, so that a row's slice of x or W is
-// one whole 128-byte line: eight consecutive lanes load one row slice
-// (16 bytes each), a wave eight whole rows per instruction.  (Loads of 32
-// bytes per row from 32 rows, in the operand's own order, measured about
-// 9 bytes per cycle per CU and bounded the kernel.)  Each stage is loaded
-// into registers two steps ahead and written, one step ahead, to the other
-// of two 64 KiB LDS buffers in the order the MFMA operands are read: per 32-row block and
-// K-16 slice a 1 KiB region holding chunk c of row r at 32 (c % 2) + r % 32,
-// so the 64 lanes of an operand read one contiguous KiB, free of bank
-// conflicts.  Rows past the batch, columns past h_out and K past h_in are
-// loads out of the buffer's range, which read zeros.
+// Pipeline: K advances in stages of 64 KiB, the x and W slices of the tile:
+// 64 of K for T = 256 (a row's slice is one whole 128-byte line), 128 for
+// T = 128 (two lines).  Consecutive lanes load consecutive 16-byte chunks of
+// one row slice, a wave whole rows per instruction.  (Loads of 32 bytes per
+// row from 32 rows, in the operand's own order, measured about 9 bytes per
+// cycle per CU and bounded the kernel.)  Each stage is loaded into registers
+// two steps ahead and written, one step ahead, to the other of two 64 KiB LDS
+// buffers in the order the MFMA operands are read: per 32-row block and K-16
+// slice a 1 KiB region holding chunk c of row r at 32 (c % 2) + r % 32 with
+// the bits 0..3 of the row flipped by 2 (c % 8) + c / 8, so the 64 lanes of an
+// operand read one contiguous KiB, free of bank conflicts, and the 16 chunks
+// a quarter wave writes fall in 16 different bank groups.  Rows past the
+// batch, columns past h_out and K past h_in are loads out of the buffer's
+// range, which read zeros.
 //
 // Epilogue: for every run of the tile's rows that share an adapter (at most
 // a few for prompt segments), B_g's ranks are staged in LDS 64 at a time,
@@ -49,9 +55,14 @@
 // (exact).  The sum is rounded once to the storage dtype.
 //
 // Tiles go to XCDs in blocks: workgroup p runs on XCD p % n_xcd and takes the
-// (p / n_xcd)-th tile of that XCD's contiguous share of the row-major tile
-// order, so the tiles an XCD runs at a time share rows of x and columns of W
-// in its L2.
+// (p / n_xcd)-th tile of that XCD's contiguous share of the tile order.  The
+// order runs over panels of kPanel row tiles, column by column inside a
+// panel, so that an XCD's share, and the part of it that runs at a time, is a
+// block of tiles a few row tiles high and a few column tiles wide: they share
+// rows of x and columns of W in the XCD's L2 (a 1024-token prompt in tiles of
+// 128: each XCD all 8 row tiles x 4 column tiles, 12 MiB of x and W, where
+// one row tile x all 32 column tiles would be 33 MiB).  Every XCD gets per_xcd workgroups (the whole tiles over n_xcd,
+// rounded up); those past the last tile end at once.
 //
 // A last round of tiles that would leave compute units idle is split along
 // K: each of its tiles runs as `split` workgroups over consecutive K ranges,
@@ -74,14 +85,26 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kStageChunks = kBaseStageBytes / 16;     // 4096 chunks of 16 bytes
 constexpr int kRegionChunks = 64;                      // one operand fragment: 32 rows x 2 chunks (K 16)
-constexpr int kKQ = kBaseBK / 16;                      // K-16 slices per stage
-constexpr int kWRegion = kKQ * (kBaseBM / 32);         // first region of the W slice in a stage
-constexpr int kRowChunks = kBaseBK / 8;                // 16-byte chunks per row of a stage
-constexpr int kRowStep = kBaseThreads / kRowChunks;    // rows between a thread's staged chunks
-constexpr int kLoads = kBaseBM / kRowStep;             // chunks of x (and of W) a thread stages
-static_assert(kBaseBK == 64 && kBaseThreads == 256 && kBaseBM == kBaseBN && kBaseBM == 256, "base tiling");
-static_assert(kLoads == 8 && kRowStep == 32, "staging");
-static_assert(kBaseLoraRanks * kBaseBN * 2 <= kBaseStageBytes, "B_g staging fits one stage buffer");
+static_assert(kBaseThreads == 256, "base tiling: 2 x 2 waves");
+
+// Derived tiling of tile edge T.
+template <int T>
+struct BaseCfg {
+    static constexpr int kBK = base_bk(T);                   // K per stage
+    static constexpr int kKQ = kBK / 16;                     // K-16 slices per stage
+    static constexpr int kWB = T / 64;                       // 32 x 32 blocks per wave and dimension
+    static constexpr int kWRegion = kKQ * (T / 32);          // first region of the W slice in a stage
+    static constexpr int kRowChunks = kBK / 8;               // 16-byte chunks per row of a stage
+    static constexpr int kRowStep = kBaseThreads / kRowChunks;   // rows between a thread's staged chunks
+    static constexpr int kLoads = T / kRowStep;              // chunks of x (and of W) a thread stages
+    static constexpr int kTileQuads = T * T / 4;
+    // K-16 slices whose fragments are read ahead of the MFMAs: the small
+    // tile's 4 MFMAs per slice do not cover one LDS read's latency
+    static constexpr int kAhead = T == 256 ? 1 : 2;
+    static_assert(kLoads == 8 && kKQ % 4 == 0 && kRowStep % 16 == 0, "staging");
+    static_assert(kWRegion * 2 * kRegionChunks == kStageChunks, "a stage fills its buffer");
+    static_assert(kBaseLoraRanks * T * 2 <= kBaseStageBytes, "B_g staging fits one stage buffer");
+};
 
 // s_waitcnt lgkmcnt(0), vmcnt and expcnt left free (gfx9 encoding).
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
@@ -107,144 +130,165 @@ __device__ __forceinline__ f32x16 mma32x32<FmtBF16>(const u32x4& a, const u32x4&
                                                    c, 0, 0, 0);
 }
 
-template <class Fmt>
+// Row tile mt and column tile nt of tile index `tile` in the panel order.
+constexpr int kPanel = 8;
+__device__ __forceinline__ void tile_coords(const BaseArgs& a, int tile, int& mt, int& nt) {
+    const int per_panel = kPanel * a.n_nt;
+    const int panel = tile / per_panel;
+    const int h = min_i(kPanel, a.n_mt - panel * kPanel);   // row tiles of this panel
+    const int u = tile - panel * per_panel;
+    nt = u / h;
+    mt = panel * kPanel + (u - nt * h);
+}
+
+// Bits 0..3 of a staged row's place in its region are flipped by swz(c) for
+// chunk c of the row.
+__device__ __forceinline__ int swz(int c) { return 2 * (c & 7) + (c >> 3); }
+
+template <class Fmt, int TILE>
 struct BaseTile {
+    using C = BaseCfg<TILE>;
+    static constexpr int WB = C::kWB;
     const BaseArgs& a;
     const int t, w, l, wm, wn;
     const int m0, n0;
     rsrc_t xr, wr;
-    // this thread stages chunk c = t % 8 of rows r0 + 32 i (i < 8) of x and of W
+    // this thread stages chunk c = t % kRowChunks of rows r0 + kRowStep i
+    // (i < 8) of x and of W
     int c;
-    uint32_t xo[kLoads], wo[kLoads];       // byte offsets at K = 0; kOut for rows past the matrix
-    int lpos;                              // LDS chunk of row r0 (region, swizzled lane)
-    u32x4 st[2][kLoads][2];                // the next two stages, in flight: [stage parity][i][x, W]
-    f32x16 acc[4][4];                      // [32-row block of x][32-column block of y]
+    uint32_t xo[C::kLoads], wo[C::kLoads];   // byte offsets at K = 0; kOut for rows past the matrix
+    int lpos;                                // LDS chunk of row r0 (region, swizzled lane)
+    u32x4 st[2][C::kLoads][2];               // the next two stages, in flight: [stage parity][i][x, W]
+    f32x16 acc[WB][WB];                      // [32-row block of x][32-column block of y]
 
     __device__ __forceinline__ BaseTile(const BaseArgs& args, int mt, int nt)
         : a(args), t(threadIdx.x), w(threadIdx.x >> 6), l(threadIdx.x & 63), wm((threadIdx.x >> 6) >> 1),
-          wn((threadIdx.x >> 6) & 1), m0(mt * kBaseBM), n0(nt * kBaseBN) {
+          wn((threadIdx.x >> 6) & 1), m0(mt * TILE), n0(nt * TILE) {
         xr = make_rsrc(a.x, a.x_bytes);
         wr = make_rsrc(a.wt, a.w_bytes);
-        const int r0 = t / kRowChunks;
-        c = t % kRowChunks;
+        const int r0 = t / C::kRowChunks;
+        c = t % C::kRowChunks;
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
-            const int row = m0 + r0 + kRowStep * i, col = n0 + r0 + kRowStep * i;
+        for (int i = 0; i < C::kLoads; ++i) {
+            const int row = m0 + r0 + C::kRowStep * i, col = n0 + r0 + C::kRowStep * i;
             xo[i] = row < a.M ? (uint32_t)(((int64_t)row * a.ldx) * 2) + 16u * c : (uint32_t)kOut;
             wo[i] = col < a.N ? (uint32_t)(((int64_t)col * a.ldw) * 2) + 16u * c : (uint32_t)kOut;
         }
-        // chunk c of row r goes to region (r / 32, c / 2) at 32 (c % 2) + r % 32,
-        // its bits 1..3 flipped by 2c; rows r0 + 32 i are region rows i apart
-        lpos = (c >> 1) * kRegionChunks + ((32 * (c & 1) + r0) ^ (2 * c));
+        // chunk c of row r goes to region (r / 32, c / 2) at 32 (c % 2) + r % 32
+        // with bits 0..3 flipped by swz(c); row r0 + kRowStep i is kRowStep i
+        // rows further (swz leaves bit 4 alone)
+        lpos = (c >> 1) * kRegionChunks + ((32 * (c & 1) + r0) ^ swz(c));
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < WB; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < WB; ++j)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     }
 
-    // Stage k of x (part 0) or W (part 1) into staging set S: eight
-    // consecutive lanes read one 128-byte row slice, a wave eight whole rows
-    // per instruction.  Stages past K read zeros.
-    template <int S, int part>
+    // Chunks [I0, I1) of stage k of x (part 0) or W (part 1) into staging
+    // set S: consecutive lanes read consecutive 16-byte chunks of one row
+    // slice, a wave whole rows per instruction.  Stages past K read zeros.
+    template <int S, int part, int I0 = 0, int I1 = C::kLoads>
     __device__ __forceinline__ void load(int k) {
         // one select per stage: K past the end moves every offset past the
         // buffer (offsets and kOut stay below 2^32 together, above its size)
-        const uint32_t kb = k * kBaseBK + 8 * c < a.K ? (uint32_t)k * (kBaseBK * 2) : (uint32_t)kOut;
+        const uint32_t kb = k * C::kBK + 8 * c < a.K ? (uint32_t)k * (C::kBK * 2) : (uint32_t)kOut;
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) st[S][i][part] = bload16(part ? wr : xr, (int)((part ? wo[i] : xo[i]) + kb));
+        for (int i = I0; i < I1; ++i) st[S][i][part] = bload16(part ? wr : xr, (int)((part ? wo[i] : xo[i]) + kb));
     }
 
-    // The staged part 0 (x) or 1 (W) into buf in the operand order.  The
-    // 16 chunks a quarter wave writes (two rows, eight chunks each) fall in 16
-    // different bank groups; a reader's 16 consecutive lanes share c and stay
-    // in one aligned group of 16 chunks.
-    template <int S, int part>
+    // Staged chunks [I0, I1) of part 0 (x) or 1 (W) into buf in the operand
+    // order.  The 16 chunks a quarter wave writes fall in 16 different bank
+    // groups; a reader's 16 consecutive lanes share c and stay in one aligned
+    // group of 16 chunks.
+    template <int S, int part, int I0 = 0, int I1 = C::kLoads>
     __device__ __forceinline__ void commit(u32x4* buf) {
 #pragma unroll
-        for (int i = 0; i < kLoads; ++i) buf[(part ? kWRegion : 0) * kRegionChunks + i * (kKQ * kRegionChunks) + lpos] =
-            st[S][i][part];
+        for (int i = I0; i < I1; ++i) {
+            constexpr int kRegionRow = C::kKQ * kRegionChunks;   // chunks between 32-row blocks
+            const int rr = C::kRowStep * i;
+            buf[(part ? C::kWRegion : 0) * kRegionChunks + (rr / 32) * kRegionRow + rr % 32 + lpos] = st[S][i][part];
+        }
     }
 
-    // Operand fragments of K-16 slice q: W blocks 4 wn + j into f[0..3], x
-    // blocks 4 wm + i into f[4..7].
+    // Operand fragments of K-16 slice q: W blocks WB wn + j into f[j], x
+    // blocks WB wm + i into f[WB + i].
     __device__ __forceinline__ void frags(const u32x4* buf, int q, u32x4* f) {
-        const int ls = (l ^ (2 * (l >> 5))) ^ (4 * q);   // lane l reads chunk 2q + l / 32 of its rows
+        // lane l reads chunk 2q + l / 32 of row l % 32 of its blocks
+        const int ls = l ^ (4 * (q & 3) + 2 * (l >> 5) + (q >> 2));
 #pragma unroll
-        for (int j = 0; j < 4; ++j) f[j] = buf[(kWRegion + kKQ * (4 * wn + j) + q) * kRegionChunks + ls];
+        for (int j = 0; j < WB; ++j) f[j] = buf[(C::kWRegion + C::kKQ * (WB * wn + j) + q) * kRegionChunks + ls];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) f[4 + i] = buf[(kKQ * (4 * wm + i) + q) * kRegionChunks + ls];
+        for (int i = 0; i < WB; ++i) f[WB + i] = buf[(C::kKQ * (WB * wm + i) + q) * kRegionChunks + ls];
     }
 
     __device__ __forceinline__ void mfmas(const u32x4* f) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < WB; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = mma32x32<Fmt>(f[j], f[4 + i], acc[i][j]);
+            for (int j = 0; j < WB; ++j) acc[i][j] = mma32x32<Fmt>(f[j], f[WB + i], acc[i][j]);
+    }
+
+    // Slice s of step k: the fragment reads of slice s + kAhead, this
+    // slice's share of the step's memory work, the slice's MFMAs.  The memory work is
+    // in four parts, each over a quarter of the slices: the writes of stage
+    // k + 1's x, then of its W (loaded during step k - 1) into nxt, whose
+    // readers have passed the barrier, then the loads of stage k + 3's x,
+    // then of its W.
+    static constexpr int NF = C::kAhead + 1;       // fragment sets in registers
+    template <int P, int s>
+    __device__ __forceinline__ void slices(const u32x4* cur, u32x4* nxt, int k, u32x4 (&f)[NF][2 * WB]) {
+        constexpr int NQ = C::kKQ / 4;
+        constexpr int kind = s / NQ;
+        constexpr int NO = C::kLoads / NQ;         // memory instructions of the slice
+        constexpr int I0 = (s % NQ) * NO;
+        constexpr bool reads = s + C::kAhead < C::kKQ;
+        constexpr int NM = WB * WB / NO;           // MFMAs per memory instruction
+        if constexpr (reads) frags(cur, s + C::kAhead, f[(s + C::kAhead) % NF]);
+        if constexpr (kind == 0) commit<P ^ 1, 0, I0, I0 + NO>(nxt);
+        else if constexpr (kind == 1) commit<P ^ 1, 1, I0, I0 + NO>(nxt);
+        else if constexpr (kind == 2) load<P ^ 1, 0, I0, I0 + NO>(k + 3);
+        else load<P ^ 1, 1, I0, I0 + NO>(k + 3);
+        mfmas(f[s % NF]);
+        constexpr int op = kind < 2 ? kSchedDsWrite : kSchedVmemRead;
+        static_assert(NM >= 1 && (!reads || 2 * WB == NO), "slice schedule");
+#pragma unroll
+        for (int g = 0; g < NO; ++g) {
+            if constexpr (reads) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                if constexpr (NM > 1) __builtin_amdgcn_sched_group_barrier(kSchedMfma, NM - 1, 0);
+            } else {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, NM, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(op, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (s + 1 < C::kKQ) slices<P, s + 1>(cur, nxt, k, f);
     }
 
     // Step k on buffer cur (stage k, written in step k-1).  Every wave's
     // writes of stage k and reads of stage k-1 are done at the barrier; then
-    // the 64 MFMAs run with, in their shadow, the fragment reads of the next
-    // K slice, the writes of stage k+1 (loaded during step k-1) into nxt,
-    // whose readers have passed the barrier, and the loads of stage k+2.
+    // the MFMAs run with, in their shadow, the fragment reads of the K slices
+    // ahead and the step's memory work.
     template <int P>
     __device__ __forceinline__ void step(const u32x4* cur, u32x4* nxt, int k) {
         wait_lgkm0();
         __builtin_amdgcn_s_barrier();
-        u32x4 f[2][8];
-        frags(cur, 0, f[0]);
+        u32x4 f[NF][2 * WB];
+#pragma unroll
+        for (int q = 0; q < C::kAhead; ++q) frags(cur, q, f[q]);
         __builtin_amdgcn_sched_barrier(0);
-        // slice 0: 16 MFMAs, with the fragment reads of slice 1 and the x
-        // writes of stage k+1 between them
-        frags(cur, 1, f[1]);
-        commit<P ^ 1, 0>(nxt);
-        mfmas(f[0]);
-        for (int g = 0; g < 8; ++g) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        // slice 1: reads of slice 2, W writes of stage k+1
-        frags(cur, 2, f[0]);
-        commit<P ^ 1, 1>(nxt);
-        mfmas(f[1]);
-        for (int g = 0; g < 8; ++g) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        // slice 2: reads of slice 3, x loads of stage k+3
-        frags(cur, 3, f[1]);
-        load<P ^ 1, 0>(k + 3);
-        mfmas(f[0]);
-        for (int g = 0; g < 8; ++g) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        // slice 3: W loads of stage k+3
-        load<P ^ 1, 1>(k + 3);
-        mfmas(f[1]);
-        for (int g = 0; g < 8; ++g) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        slices<P, 0>(cur, nxt, k, f);
     }
 };
 
 // The adapter delta of one run of rows [lo, hi) with adapter g, ranks staged
 // 64 at a time in bt (one stage buffer).
-template <class Fmt>
-__device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc, u32x4* bt) {
+template <class Fmt, int TILE>
+__device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePiece& pc, u32x4* bt) {
+    constexpr int WB = BaseTile<Fmt, TILE>::WB;
     const BaseArgs& a = T.a;
     const DevAdapter ad = a.table[pc.adapter];
     const int R = ad.rank;
@@ -261,9 +305,9 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
         // few registers beside the accumulators).
         __builtin_amdgcn_s_barrier();             // earlier readers of bt are done (every wave waited lgkmcnt)
         uint16_t* bt16 = (uint16_t*)bt;
-        for (int task = T.t; task < 8 * RC * (kBaseBN / 8); task += kBaseThreads) {
-            const int jr = task / (kBaseBN / 8);  // rank within the staged range
-            const int co = task - jr * (kBaseBN / 8);
+        for (int task = T.t; task < 8 * RC * (TILE / 8); task += kBaseThreads) {
+            const int jr = task / (TILE / 8);     // rank within the staged range
+            const int co = task - jr * (TILE / 8);
             const int j = rc0 + jr;
             const int col = T.n0 + 8 * co;
             const u32x4 b8 = bload16(br, j < R && col < a.N ? (int)((((int64_t)j * a.N) + col) * 2) : kOut);
@@ -276,12 +320,12 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
             }
         }
         __syncthreads();
-        // v operand of block i, chunk c: lane l takes row m0 + 128 wm + 32 i + (l % 32),
+        // v operand of block i, chunk c: lane l takes row m0 + TILE/2 wm + 32 i + (l % 32),
         // ranks rc0 + 8 c .. +7, the high part of s_g v for l < 32 and the low
         // part for l >= 32 (the B_g operand holds the same ranks in both
         // halves of K).  Rows outside [lo, hi) and ranks >= R read zero.
         auto vload = [&](int i, int c, f32x4& v0, f32x4& v1) __attribute__((always_inline)) {
-            const int m = T.m0 + 128 * T.wm + 32 * i + (l & 31);
+            const int m = T.m0 + (TILE / 2) * T.wm + 32 * i + (l & 31);
             const int j = rc0 + 8 * c;
             const bool ok = m >= pc.lo && m < pc.hi && j < R;
             const int off = ok ? (int)((((int64_t)m * a.ldv) + j) * 4) : kOut;
@@ -302,7 +346,7 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
         float unscale = 1.f;
         if constexpr (Fmt::kNarrowRange) {
             float vabs = 0.f;
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < WB; ++i)
                 for (int c = 0; c < RC; ++c) {
                     f32x4 v0, v1;
                     vload(i, c, v0, v1);
@@ -319,18 +363,18 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
                 vmul = ad.scale * down;
                 unscale = __uint_as_float((uint32_t)(127 - k) << 23);
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < WB; ++i)
 #pragma unroll
-                    for (int jn = 0; jn < 4; ++jn) T.acc[i][jn] *= down;
+                    for (int jn = 0; jn < WB; ++jn) T.acc[i][jn] *= down;
             }
         }
         const bool hi_half = l < 32;
         for (int c = 0; c < RC; ++c) {
-            u32x4 bf[4];
+            u32x4 bf[WB];
 #pragma unroll
-            for (int jn = 0; jn < 4; ++jn) bf[jn] = bt[(4 * T.wn + jn) * (32 * RC) + 32 * c + (l & 31)];
+            for (int jn = 0; jn < WB; ++jn) bf[jn] = bt[(WB * T.wn + jn) * (32 * RC) + 32 * c + (l & 31)];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < WB; ++i) {
                 f32x4 v0, v1;
                 vload(i, c, v0, v1);
                 v0 *= vmul;
@@ -347,45 +391,48 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt>& T, const BasePiece& pc
                                Fmt::pack2(v1[2] - Fmt::to_f32(lo16(h3)), v1[3] - Fmt::to_f32(hi16(h3)))};
                 }
 #pragma unroll
-                for (int jn = 0; jn < 4; ++jn) T.acc[i][jn] = mma32x32<Fmt>(bf[jn], vf, T.acc[i][jn]);
+                for (int jn = 0; jn < WB; ++jn) T.acc[i][jn] = mma32x32<Fmt>(bf[jn], vf, T.acc[i][jn]);
             }
         }
         if constexpr (Fmt::kNarrowRange) {
             if (unscale != 1.f) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < WB; ++i)
 #pragma unroll
-                    for (int jn = 0; jn < 4; ++jn) T.acc[i][jn] *= unscale;
+                    for (int jn = 0; jn < WB; ++jn) T.acc[i][jn] *= unscale;
             }
         }
         wait_vm0_lgkm0();                         // this wave's reads of bt are done before the next staging
     }
 }
 
-template <class Fmt>
+template <class Fmt, int TILE>
 __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) {
+    using C = BaseCfg<TILE>;
+    constexpr int WB = C::kWB;
     __shared__ __attribute__((aligned(16))) u32x4 s0[kStageChunks];
     __shared__ __attribute__((aligned(16))) u32x4 s1[kStageChunks];
     // an even number of stages (a stage past K reads zeros and adds nothing),
     // so that the loop runs whole pairs of steps and has one exit
-    const int nk = ((a.K + 2 * kBaseBK - 1) / (2 * kBaseBK)) * 2;
+    const int nk = ((a.K + 2 * C::kBK - 1) / (2 * C::kBK)) * 2;
     const int p = blockIdx.x;
+    const int slots = a.n_xcd * a.per_xcd;   // workgroups of the whole tiles, per_xcd for every XCD
     int tile, k0 = 0, k1 = nk, range = -1;
-    if (p < a.n_whole) {
+    if (p < slots) {
         const int q = p / a.n_xcd;
         tile = (p - q * a.n_xcd) * a.per_xcd + q;
-        if (q >= a.per_xcd || tile >= a.n_whole) return;
+        if (tile >= a.n_whole) return;
     } else {
-        const int u = p - a.n_whole;
+        const int u = p - slots;
         tile = a.n_whole + u / a.split;
         range = u - (tile - a.n_whole) * a.split;
         k0 = range * a.chunk;
         k1 = min_i(nk, k0 + a.chunk);
         if (tile >= a.n_mt * a.n_nt || k0 >= k1) return;
     }
-    const int mt = tile / a.n_nt;
-    const int nt = tile - mt * a.n_nt;
-    BaseTile<Fmt> T(a, mt, nt);
+    int mt, nt;
+    tile_coords(a, tile, mt, nt);
+    BaseTile<Fmt, TILE> T(a, mt, nt);
 
     T.template load<0, 0>(k0);
     T.template load<0, 1>(k0);
@@ -406,39 +453,39 @@ __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) 
         const int pe = a.piece_off[mt + 1];
         for (int pi = a.piece_off[mt]; pi < pe; ++pi) {
             const BasePiece pc = a.pieces[pi];
-            tile_delta<Fmt>(T, pc, s0);
+            tile_delta<Fmt, TILE>(T, pc, s0);
         }
     }
 
     if (range >= 0) {
         // partial tile in accumulator order: float4 g of block (i, j) of wave
-        // w, lane l at (((w 4 + i) 4 + j) 4 + g) 64 + l
-        float4* dst = (float4*)a.part + (size_t)((tile - a.n_whole) * a.split + range) * (kBaseBM * kBaseBN / 4);
+        // w, lane l at (((w WB + i) WB + j) 4 + g) 64 + l
+        float4* dst = (float4*)a.part + (size_t)((tile - a.n_whole) * a.split + range) * C::kTileQuads;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < WB; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < WB; ++j)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const f32x16& c = T.acc[i][j];
-                    dst[(((T.w * 4 + i) * 4 + j) * 4 + g) * 64 + T.l] =
+                    dst[(((T.w * WB + i) * WB + j) * 4 + g) * 64 + T.l] =
                         float4{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
                 }
         return;
     }
 
-    // y: accumulator r of block (i, j) is column n0 + 128 wn + 32 j + 8 (r / 4)
-    // + 4 (l / 32) + r % 4 of row m0 + 128 wm + 32 i + l % 32: four
+    // y: accumulator r of block (i, j) is column n0 + TILE/2 wn + 32 j + 8 (r / 4)
+    // + 4 (l / 32) + r % 4 of row m0 + TILE/2 wm + 32 i + l % 32: four
     // consecutive columns per group of four registers (8-byte stores)
     const rsrc_t yr = make_rsrc(a.y, a.y_bytes);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int m = T.m0 + 128 * T.wm + 32 * i + (T.l & 31);
+    for (int i = 0; i < WB; ++i) {
+        const int m = T.m0 + (TILE / 2) * T.wm + 32 * i + (T.l & 31);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < WB; ++j)
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int n = T.n0 + 128 * T.wn + 32 * j + 8 * g + 4 * (T.l >> 5);
+                const int n = T.n0 + (TILE / 2) * T.wn + 32 * j + 8 * g + 4 * (T.l >> 5);
                 const bool ok = m < a.M && n < a.N;
                 const f32x16& c = T.acc[i][j];
                 bstore8(u32x2{Fmt::pack2(c[4 * g], c[4 * g + 1]), Fmt::pack2(c[4 * g + 2], c[4 * g + 3])}, yr,
@@ -451,24 +498,27 @@ __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) 
 // order, rounded once and stored.  One thread per four consecutive columns of
 // one row (one float4 of every partial).
 constexpr int kReduceThreads = 256;
-constexpr int kTileQuads = kBaseBM * kBaseBN / 4;
-static_assert(kTileQuads % kReduceThreads == 0, "reduce grid");
 
-template <class Fmt>
+template <class Fmt, int TILE>
 __global__ void __launch_bounds__(kReduceThreads) lora_base_reduce_kernel(BaseArgs a) {
+    using C = BaseCfg<TILE>;
+    constexpr int WB = C::kWB;
+    static_assert(C::kTileQuads % kReduceThreads == 0, "reduce grid");
     const int gid = blockIdx.x * kReduceThreads + threadIdx.x;
-    const int rt = gid / kTileQuads;
-    const int e = gid - rt * kTileQuads;
-    const int l = e & 63, g = (e >> 6) & 3, j = (e >> 8) & 3, i = (e >> 10) & 3, w = e >> 12;
+    const int rt = gid / C::kTileQuads;
+    const int e = gid - rt * C::kTileQuads;
+    const int l = e & 63, g = (e >> 6) & 3, blk = e >> 8;
+    const int j = blk % WB, i = (blk / WB) % WB, w = blk / (WB * WB);
     const int tile = a.n_whole + rt;
     if (tile >= a.n_mt * a.n_nt) return;
-    const int mt = tile / a.n_nt, nt = tile - mt * a.n_nt;
-    const int m = mt * kBaseBM + 128 * (w >> 1) + 32 * i + (l & 31);
-    const int n = nt * kBaseBN + 128 * (w & 1) + 32 * j + 8 * g + 4 * (l >> 5);
-    const float4* src = (const float4*)a.part + (size_t)rt * a.split * kTileQuads + e;
+    int mt, nt;
+    tile_coords(a, tile, mt, nt);
+    const int m = mt * TILE + (TILE / 2) * (w >> 1) + 32 * i + (l & 31);
+    const int n = nt * TILE + (TILE / 2) * (w & 1) + 32 * j + 8 * g + 4 * (l >> 5);
+    const float4* src = (const float4*)a.part + (size_t)rt * a.split * C::kTileQuads + e;
     float4 sum = src[0];
     for (int r = 1; r < a.split; ++r) {
-        const float4 v = src[(size_t)r * kTileQuads];
+        const float4 v = src[(size_t)r * C::kTileQuads];
         sum.x += v.x;
         sum.y += v.y;
         sum.z += v.z;
@@ -480,24 +530,27 @@ __global__ void __launch_bounds__(kReduceThreads) lora_base_reduce_kernel(BaseAr
     }
 }
 
+template <class Fmt, int TILE>
+hipError_t launch_tiles(const BaseArgs& a, hipStream_t s) {
+    const int n_split = a.split > 1 ? a.n_mt * a.n_nt - a.n_whole : 0;
+    const int grid = a.n_xcd * a.per_xcd + n_split * a.split;
+    if (grid <= 0) return hipSuccess;
+    hipLaunchKernelGGL((lora_base_kernel<Fmt, TILE>), dim3(grid), dim3(kBaseThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || n_split == 0) return e;
+    const int rgrid = n_split * (BaseCfg<TILE>::kTileQuads / kReduceThreads);
+    hipLaunchKernelGGL((lora_base_reduce_kernel<Fmt, TILE>), dim3(rgrid), dim3(kReduceThreads), 0, s, a);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_base(const BaseArgs& a, int dtype, hipStream_t s) {
-    const int n_split = a.split > 1 ? a.n_mt * a.n_nt - a.n_whole : 0;
-    const int grid = a.n_whole + n_split * a.split;
-    if (grid <= 0) return hipSuccess;
-    if (dtype == 0)
-        hipLaunchKernelGGL(lora_base_kernel<FmtF16>, dim3(grid), dim3(kBaseThreads), 0, s, a);
-    else
-        hipLaunchKernelGGL(lora_base_kernel<FmtBF16>, dim3(grid), dim3(kBaseThreads), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || n_split == 0) return e;
-    const int rgrid = n_split * (kTileQuads / kReduceThreads);
-    if (dtype == 0)
-        hipLaunchKernelGGL(lora_base_reduce_kernel<FmtF16>, dim3(rgrid), dim3(kReduceThreads), 0, s, a);
-    else
-        hipLaunchKernelGGL(lora_base_reduce_kernel<FmtBF16>, dim3(rgrid), dim3(kReduceThreads), 0, s, a);
-    return hipGetLastError();
+    if (a.tile == kBaseBig)
+        return dtype == 0 ? launch_tiles<FmtF16, kBaseBig>(a, s) : launch_tiles<FmtBF16, kBaseBig>(a, s);
+    if (a.tile == kBaseSmall)
+        return dtype == 0 ? launch_tiles<FmtF16, kBaseSmall>(a, s) : launch_tiles<FmtBF16, kBaseSmall>(a, s);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace lora

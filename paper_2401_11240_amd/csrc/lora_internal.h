@@ -164,16 +164,19 @@ static_assert(sizeof(KernelArgs) <= 4096, "kernel arguments");
 
 // ---------------------------------------------------------------------------
 // Fused base projection (Eq. 1 whole): y = x W + s_g (x A_g) B_g for every
-// row, one MFMA GEMM over tiles of kBaseBM rows x kBaseBN columns, the adapter
-// delta added in the tile's epilogue from a float32 v computed beforehand.
+// row, one MFMA GEMM over square tiles of kBaseBig or kBaseSmall rows x as
+// many columns, the adapter delta added in the tile's epilogue from a float32
+// v computed beforehand.  A stage holds the tile's x and W slices over
+// kBaseStageBytes / (4 tile) of K: 64 along K for the big tile (one
+// 128-byte line per row), 128 for the small one.
 // ---------------------------------------------------------------------------
-constexpr int kBaseBM = 256;             // rows of x (tokens) per tile
-constexpr int kBaseBN = 256;             // columns of y per tile
-constexpr int kBaseBK = 64;              // K per pipeline stage (one 128-byte line per row)
-constexpr int kBaseThreads = 256;        // 4 wave64: 2 (rows) x 2 (columns), 128 x 128 each
-constexpr int kBaseStageBytes = (kBaseBM + kBaseBN) * kBaseBK * 2;   // 64 KiB: x slice, then W slice
+constexpr int kBaseBig = 256;            // tile edge while whole tiles fill the compute units
+constexpr int kBaseSmall = 128;          // tile edge of launches with fewer big tiles than compute units
+constexpr int kBaseThreads = 256;        // 4 wave64: 2 (rows) x 2 (columns), each a quarter of the tile
+constexpr int kBaseStageBytes = 64 * 1024;   // x slice, then W slice
 constexpr int kBaseMinSplitStages = 8;   // fewest K stages of a split range
 constexpr int kBaseLoraRanks = 64;       // ranks of B_g staged in LDS at a time (one stage buffer)
+LORA_HD constexpr int base_bk(int tile) { return kBaseStageBytes / (4 * tile); }
 
 // One run of a tile's rows that share an adapter (g >= 0): rows [lo, hi).
 struct BasePiece {
@@ -190,15 +193,16 @@ struct BaseArgs {
     const BasePiece* pieces;
     int64_t ldx, ldw, ldy, ldv;
     int32_t M, N, K;               // rows, h_out, h_in
+    int32_t tile;                  // tile edge: kBaseBig or kBaseSmall
     int32_t n_mt, n_nt;            // row tiles, column tiles
-    int32_t n_xcd, per_xcd;        // XCDs, whole tiles per XCD
+    int32_t n_xcd, per_xcd;        // XCDs, whole tiles per XCD (rounded up): n_xcd per_xcd workgroups
     // Tiles [0, n_whole) run whole, one workgroup each.  Each tile of
     // [n_whole, n_mt n_nt) is split into `split` K ranges of `chunk` stages
-    // (workgroup n_whole + (tile - n_whole) split + s takes range s), which
+    // (workgroup n_xcd per_xcd + (tile - n_whole) split + s takes range s), which
     // write float32 partial tiles to `part`; a second kernel adds them in the
     // order of s, rounds and stores.  Range 0 carries the adapter delta.
     int32_t n_whole, split, chunk;
-    float* part;                   // [(n_mt n_nt - n_whole) split][kBaseBM kBaseBN] in accumulator order
+    float* part;                   // [(n_mt n_nt - n_whole) split][tile tile] in accumulator order
     uint32_t x_bytes, w_bytes, y_bytes, v_bytes;
     int32_t b_span_ok;             // 1: every B_g spans < 2 GiB (checked on the host)
 };

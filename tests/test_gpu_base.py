@@ -1,7 +1,9 @@
 """The fused base projection (Eq. 1 whole: y = round(x.W + s_g (x.A_g).B_g))
 through the C ABI against the oracle, element by element.
 
-Cases: ragged shapes (K and h_out not multiples of the tile), ranks that
+Cases: ragged shapes (K and h_out not multiples of the tile), both tile
+sizes (256 while whole tiles of 256 fill the compute units, 128 otherwise),
+each with its last tiles split along K, ranks that
 need several 64-rank passes and ranks that are not multiples of 8, segments
 without an adapter, several adapters in one row tile, binary16 intermediates
 past 2^15, the single 1024-token prompt on every row, and the 16-segment
@@ -99,6 +101,15 @@ SMALL = [
     (1, W.BF16, 520, 776, [8, 3, 128, 256], [1, 37, 300, 5, 1, 60], [0, 1, 2, -1, 3, 2]),
     (2, W.F16, 1032, 264, [16, 64, 40], [200, 56, 1, 1, 1, 3], [0, 1, 2, 0, -1, 1]),
     (3, W.BF16, 64, 8, [1, 2], [3, 250, 9], [1, 0, 1]),
+    # split along K: 4200 x 4104 makes 289 tiles of 256 (more than the 256
+    # compute units: the big tile, its last 33 tiles in two K ranges); 500 x
+    # 3896 makes 8 of 256 (the small tile: 124 tiles in two K ranges); both
+    # ragged in rows, columns and K, adapter runs crossing tile edges
+    (5, W.BF16, 1032, 4104, [64, 8, 40], [1500, 700, 3, 1997], [0, 1, -1, 2]),
+    (6, W.F16, 2056, 3896, [16, 128, 24], [130, 1, 250, 119], [1, 0, 2, 1]),
+    # 289 whole tiles of 256 (K too short to split): a number of whole tiles
+    # that the XCDs do not share evenly (so do cases 0 and 1, in tiles of 128)
+    (7, W.BF16, 520, 4104, [32, 8], [2100, 2100], [0, 1]),
 ]
 
 
