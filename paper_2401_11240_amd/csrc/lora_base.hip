@@ -285,10 +285,14 @@ struct BaseTile {
 };
 
 // The adapter delta of one run of rows [lo, hi) with adapter g, ranks staged
-// 64 at a time in bt (one stage buffer).
+// 64 at a time: B_g's in bt, v's in vt (the two stage buffers).  Every load
+// of a rank range is issued before any of its LDS writes, so that the range
+// costs one round trip to memory, not one per loop turn.
 template <class Fmt, int TILE>
-__device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePiece& pc, u32x4* bt) {
+__device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePiece& pc, u32x4* bt, u32x4* vt) {
     constexpr int WB = BaseTile<Fmt, TILE>::WB;
+    constexpr int kBTasks = kBaseLoraRanks * (TILE / 8) / kBaseThreads;   // B_g loads per thread (64 ranks)
+    constexpr int kVTasks = TILE * (kBaseLoraRanks / 4) / kBaseThreads;    // v loads per thread
     const BaseArgs& a = T.a;
     const DevAdapter ad = a.table[pc.adapter];
     const int R = ad.rank;
@@ -301,41 +305,90 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePie
         // B_g ranks [rc0, rc0 + 8 RC) of the tile's columns into bt: column n
         // of 32-column block nb, chunk c (ranks rc0 + 8c .. +7) at
         // nb * 32 RC + 32 c + (n % 32).  A thread loads 8 columns of one rank
-        // (16 bytes) and writes each element to its place (2-byte LDS writes:
-        // few registers beside the accumulators).
-        __builtin_amdgcn_s_barrier();             // earlier readers of bt are done (every wave waited lgkmcnt)
-        uint16_t* bt16 = (uint16_t*)bt;
-        for (int task = T.t; task < 8 * RC * (TILE / 8); task += kBaseThreads) {
-            const int jr = task / (TILE / 8);     // rank within the staged range
-            const int co = task - jr * (TILE / 8);
-            const int j = rc0 + jr;
-            const int col = T.n0 + 8 * co;
-            const u32x4 b8 = bload16(br, j < R && col < a.N ? (int)((((int64_t)j * a.N) + col) * 2) : kOut);
+        // (16 bytes) and writes each element to its place (2-byte LDS writes).
+        // (the big tile, short of registers beside its accumulators, stages
+        // B_g and v in two halves each: a half's loads after the previous
+        // half's writes)
+        constexpr int kHalves = TILE == kBaseBig ? 2 : 1;
+        constexpr int kBLoads = kBTasks / kHalves;
+        u32x4 b8[kBLoads];
+        auto bfetch = [&](int h) __attribute__((always_inline)) {
 #pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const int n = 8 * co + c;
-                const uint32_t word = b8[c >> 1];
-                bt16[((n >> 5) * (32 * RC) + 32 * (jr >> 3) + (n & 31)) * 8 + (jr & 7)] =
-                    (uint16_t)((c & 1) ? hi16(word) : lo16(word));
+            for (int it = 0; it < kBLoads; ++it) {
+                const int task = T.t + (h * kBLoads + it) * kBaseThreads;
+                const int jr = task / (TILE / 8);     // rank within the staged range
+                const int j = rc0 + jr;
+                const int col = T.n0 + 8 * (task - jr * (TILE / 8));
+                b8[it] = bload16(br, jr < 8 * RC && j < R && col < a.N ? (int)((((int64_t)j * a.N) + col) * 2) : kOut);
             }
+        };
+        uint16_t* bt16 = (uint16_t*)bt;
+        auto bstore = [&](int h) __attribute__((always_inline)) {
+#pragma unroll
+            for (int it = 0; it < kBLoads; ++it) {
+                const int task = T.t + (h * kBLoads + it) * kBaseThreads;
+                const int jr = task / (TILE / 8);
+                const int co = task - jr * (TILE / 8);
+                if (jr < 8 * RC) {
+#pragma unroll
+                    for (int c = 0; c < 8; ++c) {
+                        const int n = 8 * co + c;
+                        const uint32_t word = b8[it][c >> 1];
+                        bt16[((n >> 5) * (32 * RC) + 32 * (jr >> 3) + (n & 31)) * 8 + (jr & 7)] =
+                            (uint16_t)((c & 1) ? hi16(word) : lo16(word));
+                    }
+                }
+            }
+        };
+        // v of the tile's rows for ranks [rc0, rc0 + 64) into vt: float4 q
+        // (ranks rc0 + 4q .. +3) of tile row r at 16 r + (q ^ (r % 16)), so
+        // that 16 lanes reading one chunk of 16 rows hit 16 bank groups.
+        // Rows outside [lo, hi) and ranks >= R are zeros.
+        constexpr int kVLoads = kVTasks / kHalves;
+        f32x4 vv[kVLoads];
+        auto vfetch = [&](int h) __attribute__((always_inline)) {
+#pragma unroll
+            for (int it = 0; it < kVLoads; ++it) {
+                const int e = T.t + (h * kVLoads + it) * kBaseThreads;
+                const int m = T.m0 + (e >> 4);
+                const int j = rc0 + 4 * (e & 15);
+                const bool ok = m >= pc.lo && m < pc.hi && j < R;
+                vv[it] = as_f4(bload16(vr, ok ? (int)((((int64_t)m * a.ldv) + j) * 4) : kOut));
+            }
+        };
+        f32x4* vt4 = (f32x4*)vt;
+        auto vstore = [&](int h) __attribute__((always_inline)) {
+#pragma unroll
+            for (int it = 0; it < kVLoads; ++it) {
+                const int e = T.t + (h * kVLoads + it) * kBaseThreads;
+                const int r = e >> 4, q = e & 15;
+                f32x4 v = vv[it];
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (rc0 + 4 * q + k >= R) v[k] = 0.f;
+                vt4[16 * r + (q ^ (r & 15))] = v;
+            }
+        };
+        bfetch(0);
+        vfetch(0);
+        __builtin_amdgcn_s_barrier();             // earlier readers of bt and vt are done (every wave waited lgkmcnt)
+        bstore(0);
+        vstore(0);
+        if constexpr (kHalves == 2) {
+            bfetch(1);
+            vfetch(1);
+            bstore(1);
+            vstore(1);
         }
         __syncthreads();
-        // v operand of block i, chunk c: lane l takes row m0 + TILE/2 wm + 32 i + (l % 32),
-        // ranks rc0 + 8 c .. +7, the high part of s_g v for l < 32 and the low
-        // part for l >= 32 (the B_g operand holds the same ranks in both
-        // halves of K).  Rows outside [lo, hi) and ranks >= R read zero.
+        // v operand of block i, chunk c: lane l takes row TILE/2 wm + 32 i + (l % 32)
+        // of the tile, ranks rc0 + 8 c .. +7, the high part of s_g v for l < 32
+        // and the low part for l >= 32 (the B_g operand holds the same ranks in
+        // both halves of K).
         auto vload = [&](int i, int c, f32x4& v0, f32x4& v1) __attribute__((always_inline)) {
-            const int m = T.m0 + (TILE / 2) * T.wm + 32 * i + (l & 31);
-            const int j = rc0 + 8 * c;
-            const bool ok = m >= pc.lo && m < pc.hi && j < R;
-            const int off = ok ? (int)((((int64_t)m * a.ldv) + j) * 4) : kOut;
-            v0 = as_f4(bload16(vr, off));
-            v1 = as_f4(bload16(vr, off + 16));
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if (j + e >= R) v0[e] = 0.f;
-                if (j + 4 + e >= R) v1[e] = 0.f;
-            }
+            const int r = (TILE / 2) * T.wm + 32 * i + (l & 31);
+            v0 = vt4[16 * r + ((2 * c) ^ (r & 15))];
+            v1 = vt4[16 * r + ((2 * c + 1) ^ (r & 15))];
         };
         // v enters the MFMA pre-multiplied by s_g, so the delta adds straight
         // into the base accumulators.  binary16: past 2^15 the wave scales v
@@ -453,7 +506,7 @@ __global__ void __launch_bounds__(kBaseThreads, 1) lora_base_kernel(BaseArgs a) 
         const int pe = a.piece_off[mt + 1];
         for (int pi = a.piece_off[mt]; pi < pe; ++pi) {
             const BasePiece pc = a.pieces[pi];
-            tile_delta<Fmt, TILE>(T, pc, s0);
+            tile_delta<Fmt, TILE>(T, pc, s0, s1);
         }
     }
 

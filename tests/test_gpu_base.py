@@ -109,7 +109,7 @@ SMALL = [
     (6, W.F16, 2056, 3896, [16, 128, 24], [130, 1, 250, 119], [1, 0, 2, 1]),
     # 289 whole tiles of 256 (K too short to split): a number of whole tiles
     # that the XCDs do not share evenly (so do cases 0 and 1, in tiles of 128)
-    (7, W.BF16, 520, 4104, [32, 8], [2100, 2100], [0, 1]),
+    (7, W.F16, 520, 4104, [32, 8], [2100, 2100], [0, 1]),
 ]
 
 
