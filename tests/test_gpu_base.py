@@ -3,7 +3,7 @@ through the C ABI against the oracle, element by element.
 
 Cases: ragged shapes (K and h_out not multiples of the tile), both tile
 sizes (256 while whole tiles of 256 fill the compute units, 128 otherwise),
-each with its last tiles split along K, ranks that
+each with its last tiles split along K, six seeded random shapes, ranks that
 need several 64-rank passes and ranks that are not multiples of 8, segments
 without an adapter, several adapters in one row tile, binary16 intermediates
 past 2^15, the single 1024-token prompt on every row, and the 16-segment
@@ -123,6 +123,39 @@ def test_small_cases_every_row(case):
     rows = np.arange(w.n_rows)
     ref = oracle_rows(w, rows)
     st = compare(got, ref, w.dtype, f"base case {case}", mag=allowance(w, rows))
+    say("  ", st)
+    dw.release()
+
+
+def random_case(seed):
+    """A seeded random shape: rows 1..3000 in 1..8 segments (some without an
+    adapter), h_in and h_out multiples of 8 up to 2056 / 4104, ranks 1..128;
+    every third case wide enough for tiles of 256 (at least 256 of them)."""
+    rng = np.random.default_rng(1000 + seed)
+    big = seed % 3 == 2
+    n_seg = int(rng.integers(1, 9))
+    total = int(rng.integers(4100, 4400)) if big else int(rng.integers(1, 3001))
+    cuts = np.sort(rng.choice(np.arange(1, total), size=min(n_seg - 1, total - 1), replace=False)) if total > 1 else []
+    lens = np.diff(np.concatenate([[0], cuts, [total]])).astype(int).tolist()
+    n_ad = int(rng.integers(1, 5))
+    ranks = [int(r) for r in rng.integers(1, 129, size=n_ad)]
+    sa = [int(g) for g in rng.integers(-1, n_ad, size=len(lens))]
+    h_in = 8 * int(rng.integers(1, 258))
+    h_out = 8 * int(rng.integers(513, 514)) if big else 8 * int(rng.integers(1, 514))
+    dtype = W.F16 if rng.integers(0, 2) else W.BF16
+    return (2000 + seed, dtype, h_in, h_out, ranks, lens, sa)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_shapes_every_row(seed):
+    case = random_case(seed)
+    _, dtype, h_in, h_out, ranks, lens, sa = case
+    say(f"base random {seed}: dtype={dtype} h_in={h_in} h_out={h_out} ranks={ranks} lens={lens} adapters={sa}")
+    w = small_case(*case)
+    dw = D.upload(w, DEV)
+    got = run_base(dw, w)
+    rows = np.arange(w.n_rows)
+    st = compare(got, oracle_rows(w, rows), w.dtype, f"base random {seed}", mag=allowance(w, rows))
     say("  ", st)
     dw.release()
 
