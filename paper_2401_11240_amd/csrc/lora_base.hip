@@ -46,7 +46,9 @@
 // Epilogue: for every run of the tile's rows that share an adapter (at most
 // a few for prompt segments), B_g's ranks are staged in LDS 64 at a time,
 // transposed so that 8 consecutive ranks of one output column form an
-// operand slice, and each wave adds s_g v . B_g for its rows into its base
+// operand slice, with the tile's rows of v for the same ranks in the other
+// stage buffer (all loads of a rank range issued before its LDS writes), and
+// each wave adds s_g v . B_g for its rows into its base
 // accumulators: s_g v is split into a high and a low 16-bit part that share
 // one 32x32x16 MFMA (its 16 K slots hold 8 ranks twice), rows of other runs
 // masked to zero.  binary16 cannot hold a high part past 65504, so for it each
@@ -61,8 +63,9 @@
 // block of tiles a few row tiles high and a few column tiles wide: they share
 // rows of x and columns of W in the XCD's L2 (a 1024-token prompt in tiles of
 // 128: each XCD all 8 row tiles x 4 column tiles, 12 MiB of x and W, where
-// one row tile x all 32 column tiles would be 33 MiB).  Every XCD gets per_xcd workgroups (the whole tiles over n_xcd,
-// rounded up); those past the last tile end at once.
+// one row tile x all 32 column tiles would be 33 MiB).  Every XCD gets
+// per_xcd workgroups (the whole tiles over n_xcd, rounded up); those past the
+// last tile end at once.
 //
 // A last round of tiles that would leave compute units idle is split along
 // K: each of its tiles runs as `split` workgroups over consecutive K ranges,
