@@ -311,8 +311,12 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePie
         // (16 bytes) and writes each element to its place (2-byte LDS writes).
         // (the big tile, short of registers beside its accumulators, stages
         // B_g and v in two halves each: a half's loads after the previous
-        // half's writes)
-        constexpr int kHalves = TILE == kBaseBig ? 2 : 1;
+        // half's writes.  Binary16 in the big tile, whose range check keeps
+        // more registers, stages B_g one load at a time and reads v from
+        // memory per fragment: staged in bulk, it spills.)
+        constexpr bool kLean = Fmt::kNarrowRange && TILE == kBaseBig;
+        constexpr int kHalves = kLean ? kBTasks : (TILE == kBaseBig ? 2 : 1);
+        constexpr bool kVLds = !kLean;
         constexpr int kBLoads = kBTasks / kHalves;
         u32x4 b8[kBLoads];
         auto bfetch = [&](int h) __attribute__((always_inline)) {
@@ -373,15 +377,16 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePie
             }
         };
         bfetch(0);
-        vfetch(0);
+        if constexpr (kVLds) vfetch(0);
         __builtin_amdgcn_s_barrier();             // earlier readers of bt and vt are done (every wave waited lgkmcnt)
         bstore(0);
-        vstore(0);
-        if constexpr (kHalves == 2) {
-            bfetch(1);
-            vfetch(1);
-            bstore(1);
-            vstore(1);
+        if constexpr (kVLds) vstore(0);
+#pragma unroll 1
+        for (int h = 1; h < kHalves; ++h) {
+            bfetch(h);
+            if constexpr (kVLds) vfetch(h);
+            bstore(h);
+            if constexpr (kVLds) vstore(h);
         }
         __syncthreads();
         // v operand of block i, chunk c: lane l takes row TILE/2 wm + 32 i + (l % 32)
@@ -390,8 +395,22 @@ __device__ __forceinline__ void tile_delta(BaseTile<Fmt, TILE>& T, const BasePie
         // both halves of K).
         auto vload = [&](int i, int c, f32x4& v0, f32x4& v1) __attribute__((always_inline)) {
             const int r = (TILE / 2) * T.wm + 32 * i + (l & 31);
-            v0 = vt4[16 * r + ((2 * c) ^ (r & 15))];
-            v1 = vt4[16 * r + ((2 * c + 1) ^ (r & 15))];
+            if constexpr (kVLds) {
+                v0 = vt4[16 * r + ((2 * c) ^ (r & 15))];
+                v1 = vt4[16 * r + ((2 * c + 1) ^ (r & 15))];
+            } else {
+                const int m = T.m0 + r;
+                const int j = rc0 + 8 * c;
+                const bool ok = m >= pc.lo && m < pc.hi && j < R;
+                const int off = ok ? (int)((((int64_t)m * a.ldv) + j) * 4) : kOut;
+                v0 = as_f4(bload16(vr, off));
+                v1 = as_f4(bload16(vr, off + 16));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (j + e >= R) v0[e] = 0.f;
+                    if (j + 4 + e >= R) v1[e] = 0.f;
+                }
+            }
         };
         // v enters the MFMA pre-multiplied by s_g, so the delta adds straight
         // into the base accumulators.  binary16: past 2^15 the wave scales v
