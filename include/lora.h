@@ -374,6 +374,34 @@ int lora_plan_inspect(const lora_batch_t* b, int32_t h_in, int32_t h_out, int32_
                       const int32_t* ranks, int32_t n_xcd, lora_item_info_t* items, int32_t capacity,
                       int32_t* n_items);
 
+/*
+ * The schedule of the fused base GEMM (lora_base_apply) for this batch, on
+ * the host only (no GPU, no allocation): for adapters of ranks[0 ..
+ * n_adapters) on a projection h_in -> h_out and a device of n_cu compute
+ * units in n_xcd XCDs.  For inspection and tests of the tiling.  Tiles are
+ * square, of edge `tile`; K runs in n_stages stages of stage_k.  The tile
+ * order runs over panels of `panel` row tiles, column by column inside a
+ * panel; its first n_whole tiles run whole, workgroup p (p < n_xcd per_xcd)
+ * taking the (p / n_xcd)-th tile of XCD p % n_xcd's share of per_xcd
+ * consecutive tiles; each later tile runs as `split` workgroups over
+ * consecutive ranges of `chunk` stages.  workspace_bytes is
+ * lora_base_workspace_bytes'.  Errors as lora_plan_inspect's.
+ */
+typedef struct {
+    int32_t tile;               /* tile edge: 256 or 128                          */
+    int32_t n_mt, n_nt;         /* row tiles, column tiles                        */
+    int32_t n_whole;            /* tiles run whole                                */
+    int32_t split, chunk;       /* K ranges of each other tile, stages per range  */
+    int32_t n_stages, stage_k;  /* stages of K (an even number), K per stage      */
+    int32_t per_xcd;            /* whole-tile workgroups per XCD                  */
+    int32_t grid;               /* workgroups of the GEMM launch                  */
+    int32_t panel;              /* row tiles per panel of the tile order          */
+    int32_t pad;
+    uint64_t workspace_bytes;
+} lora_base_info_t;
+int lora_base_inspect(const lora_batch_t* b, int32_t h_in, int32_t h_out, int32_t n_adapters,
+                      const int32_t* ranks, int32_t n_cu, int32_t n_xcd, lora_base_info_t* out);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* lora_last_error(void);
 

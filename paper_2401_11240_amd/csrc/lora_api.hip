@@ -1168,6 +1168,50 @@ int lora_base_workspace_bytes(lora_table_t t, const lora_batch_t* b, size_t* byt
     return LORA_OK;
 }
 
+int lora_base_inspect(const lora_batch_t* b, int32_t h_in, int32_t h_out, int32_t n_adapters, const int32_t* ranks,
+                      int32_t n_cu, int32_t n_xcd, lora_base_info_t* out) {
+    if (!out) return fail(LORA_E_ARG, "out is NULL");
+    if (h_in <= 0 || h_out <= 0 || h_in % 8 || h_out % 8)
+        return fail(LORA_E_SHAPE, "h_in and h_out must be positive multiples of 8");
+    if ((uint64_t)std::max(h_in, h_out) * kMaxRank * 2 > kMaxSpan)
+        return fail(LORA_E_SHAPE, "h_in and h_out must be at most 4 Mi elements (factors below 2 GiB)");
+    if (n_adapters < 0 || (n_adapters > 0 && !ranks)) return fail(LORA_E_ARG, "bad adapter ranks");
+    if (n_cu < 0) return fail(LORA_E_ARG, "negative n_cu");
+    lora_table_s t;                           // host-side table: ranks and shapes only
+    t.h_in = h_in;
+    t.h_out = h_out;
+    t.n = n_adapters;
+    t.n_cu = n_cu;
+    t.n_xcd = std::max(1, std::min(n_xcd, 64));
+    t.host.assign(n_adapters, DevAdapter{});
+    for (int i = 0; i < n_adapters; ++i) {
+        if (ranks[i] < 1 || ranks[i] > kMaxRank)
+            return fail(LORA_E_RANK, "adapter " + std::to_string(i) + " has rank " + std::to_string(ranks[i]) +
+                                         " outside [1, 256]");
+        t.host[i].rank = ranks[i];
+        t.host[i].scale = 1.f;
+    }
+    BaseLayout L;
+    if (int rc = build_base(&t, b, L)) return rc;
+    const int bk = base_bk(L.tile);
+    const int n_tiles = L.n_mt * L.n_nt;
+    const int per_xcd = (L.n_whole + t.n_xcd - 1) / t.n_xcd;
+    const int n_split = L.split > 1 ? n_tiles - L.n_whole : 0;
+    out->tile = L.tile;
+    out->n_mt = L.n_mt;
+    out->n_nt = L.n_nt;
+    out->n_whole = L.n_whole;
+    out->split = L.split;
+    out->chunk = L.chunk;
+    out->n_stages = ((h_in + 2 * bk - 1) / (2 * bk)) * 2;
+    out->stage_k = bk;
+    out->per_xcd = per_xcd;
+    out->grid = t.n_xcd * per_xcd + n_split * L.split;
+    out->panel = kBasePanel;
+    out->workspace_bytes = L.total;
+    return LORA_OK;
+}
+
 }  // extern "C"
 
 namespace {

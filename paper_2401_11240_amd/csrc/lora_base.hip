@@ -58,7 +58,7 @@
 //
 // Tiles go to XCDs in blocks: workgroup p runs on XCD p % n_xcd and takes the
 // (p / n_xcd)-th tile of that XCD's contiguous share of the tile order.  The
-// order runs over panels of kPanel row tiles, column by column inside a
+// order runs over panels of kBasePanel row tiles, column by column inside a
 // panel, so that an XCD's share, and the part of it that runs at a time, is a
 // block of tiles a few row tiles high and a few column tiles wide: they share
 // rows of x and columns of W in the XCD's L2 (a 1024-token prompt in tiles of
@@ -134,14 +134,13 @@ __device__ __forceinline__ f32x16 mma32x32<FmtBF16>(const u32x4& a, const u32x4&
 }
 
 // Row tile mt and column tile nt of tile index `tile` in the panel order.
-constexpr int kPanel = 8;
 __device__ __forceinline__ void tile_coords(const BaseArgs& a, int tile, int& mt, int& nt) {
-    const int per_panel = kPanel * a.n_nt;
+    const int per_panel = kBasePanel * a.n_nt;
     const int panel = tile / per_panel;
-    const int h = min_i(kPanel, a.n_mt - panel * kPanel);   // row tiles of this panel
+    const int h = min_i(kBasePanel, a.n_mt - panel * kBasePanel);   // row tiles of this panel
     const int u = tile - panel * per_panel;
     nt = u / h;
-    mt = panel * kPanel + (u - nt * h);
+    mt = panel * kBasePanel + (u - nt * h);
 }
 
 // Bits 0..3 of a staged row's place in its region are flipped by swz(c) for

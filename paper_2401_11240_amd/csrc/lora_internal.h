@@ -176,6 +176,7 @@ constexpr int kBaseThreads = 256;        // 4 wave64: 2 (rows) x 2 (columns), ea
 constexpr int kBaseStageBytes = 64 * 1024;   // x slice, then W slice
 constexpr int kBaseMinSplitStages = 8;   // fewest K stages of a split range
 constexpr int kBaseLoraRanks = 64;       // ranks of B_g staged in LDS at a time (one stage buffer)
+constexpr int kBasePanel = 8;            // row tiles per panel of the tile order
 LORA_HD constexpr int base_bk(int tile) { return kBaseStageBytes / (4 * tile); }
 
 // One run of a tile's rows that share an adapter (g >= 0): rows [lo, hi).

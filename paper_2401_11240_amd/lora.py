@@ -43,7 +43,7 @@ EXPORTS = (
     "lora_plan_create_multi", "lora_plan_apply_multi",
     "lora_base_workspace_bytes", "lora_base_apply", "lora_base_plan_create", "lora_base_plan_apply",
     "lora_base_plan_destroy",
-    "lora_group_rows", "lora_plan_inspect", "lora_last_error", "lora_abi_version",
+    "lora_group_rows", "lora_plan_inspect", "lora_base_inspect", "lora_last_error", "lora_abi_version",
 )
 
 
@@ -124,6 +124,7 @@ def load():
         "lora_plan_set_spin_limit": [vp, i32],
         "lora_group_rows": [C.POINTER(_Batch), i32, i32p, i32p, i32p, i32p],
         "lora_plan_inspect": [C.POINTER(_Batch), i32, i32, i32, i32p, i32, vp, i32, i32p],
+        "lora_base_inspect": [C.POINTER(_Batch), i32, i32, i32, i32p, i32, i32, vp],
         "lora_last_error": [],
         "lora_abi_version": [],
     }
@@ -325,6 +326,23 @@ def lora_group_rows(batch: Batch, n_adapters: int):
 ITEM_INFO = np.dtype([("kind", np.int32), ("row_block", np.int32), ("rank", np.int32),
                       ("nrows", np.int32), ("lo", np.int32), ("len", np.int32), ("sub", np.int32),
                       ("nsplit", np.int32), ("pstride", np.int32), ("grid_pos", np.int32)])
+
+
+# lora_base_info_t, field for field
+BASE_INFO = np.dtype([("tile", np.int32), ("n_mt", np.int32), ("n_nt", np.int32), ("n_whole", np.int32),
+                      ("split", np.int32), ("chunk", np.int32), ("n_stages", np.int32), ("stage_k", np.int32),
+                      ("per_xcd", np.int32), ("grid", np.int32), ("panel", np.int32), ("pad", np.int32),
+                      ("workspace_bytes", np.uint64)])
+
+
+def lora_base_inspect(batch: Batch, h_in: int, h_out: int, ranks: Sequence[int], n_cu: int, n_xcd: int) -> dict:
+    """The fused base GEMM's schedule for this batch (host only), as a dict
+    with the fields of lora_base_info_t."""
+    r = np.ascontiguousarray(ranks, dtype=np.int32)
+    out = np.zeros(1, dtype=BASE_INFO)
+    _check(load().lora_base_inspect(batch.c, h_in, h_out, len(r), r.ctypes.data_as(C.POINTER(C.c_int32)), n_cu,
+                                    n_xcd, out.ctypes.data))
+    return {k: int(out[0][k]) for k in BASE_INFO.names if k != "pad"}
 
 
 def lora_plan_inspect(batch: Batch, h_in: int, h_out: int, ranks: Sequence[int], n_xcd: int = 1):
