@@ -46,9 +46,9 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, datasheet
 # 262,144.0 KiB: x 1.0).  Valid only for the kernel sources it was taken on
 # (hash of csrc/*); reported as null otherwise.
 MEASURED_TRAFFIC = {
-    "sources_sha256_16": "b189dd06ff88ac46",
+    "sources_sha256_16": "2e0c8a031a8f851b",
     "workload": "decode_q4096_t64_mixed_rank_f16",
-    "fetch_kib": 6708.1, "fetch_scale": 262144.0 / 131094.4,
+    "fetch_kib": 6707.1, "fetch_scale": 262144.0 / 131093.7,
     "write_kib": 732.9, "write_scale": 1.0,
 }
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16
