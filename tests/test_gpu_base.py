@@ -160,6 +160,22 @@ def test_random_shapes_every_row(seed):
     dw.release()
 
 
+def test_host_schedule_matches_the_device_plan():
+    """lora_base_inspect, given this device's compute units, plans the same
+    workspace as lora_base_workspace_bytes on a table of the device (the tile
+    edge and the K split decide the partial-tile space)."""
+    n_cu = torch.cuda.get_device_properties(DEV).multi_processor_count
+    for case in [SMALL[0], SMALL[3], SMALL[4], random_case(2)]:
+        w = small_case(*case)
+        dw = D.upload(w, DEV)
+        p = dw.projection("proj")
+        pr = w.projection("proj")
+        info = L.lora_base_inspect(L.Batch(w.seg_offset, w.seg_adapter), pr.h_in, pr.h_out, w.ranks, n_cu, 8)
+        assert info["workspace_bytes"] == L.lora_base_workspace_bytes(p.table, dw.batch), (case[0], info)
+        say(f"  case seed {case[0]}: tile {info['tile']}, split {info['split']}, grid {info['grid']}")
+        dw.release()
+
+
 def test_rows_without_adapter_are_the_plain_product_and_empty_batch():
     w = small_case(4, W.BF16, 256, 512, [8], [100, 30], [-1, -1])
     dw = D.upload(w, DEV)
